@@ -1,0 +1,303 @@
+/*
+ * agft_oracle.c -- CPU fp64 oracle of the AGFT contextual-bandit step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may load, link or
+ * call this file; only the tests, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no code, header or constant with the GPU
+ * path.
+ *
+ * What it computes (disjoint LinUCB over the frequency arms, Sec. 4.2), for
+ * every tuner instance independently, in double precision:
+ *
+ *   A_k = lambda I + sum over past steps s with a_s = k of x_s x_s^T   (Eq. 3)
+ *   b_k =            sum over past steps s with a_s = k of r_s x_s     (Eq. 4)
+ *   theta_k = A_k^{-1} b_k                                             (Eq. 5)
+ *   UCB_k = theta_k^T x_t + alpha_t sqrt(x_t^T A_k^{-1} x_t)           (Eq. 1)
+ *   LCB_k = theta_k^T x_t - alpha_t sqrt(x_t^T A_k^{-1} x_t)
+ *   a_t   = lowest index among the active arms with the largest UCB_k  (Eq. 1)
+ *
+ * Readings where the paper is silent: A_k starts at lambda I and b_k at 0;
+ * alpha_t is alpha0 or alpha0 / sqrt(t + 1); ties go to the lowest arm index;
+ * a negative rounding of the quadratic form is taken as 0 under the root.
+ *
+ * Pruning (the confidence-bound rule of the workloads; motivation in Sec. 4.3,
+ * where pruned arms leave the action space for good): at a step t > 0 with
+ * t % period == 0, an active arm k stays active iff UCB_k >= max over the
+ * active arms j of LCB_j, all scores taken with that step's x_t and alpha_t,
+ * before that step's argmax.
+ *
+ * The paper gives the update as Eq. 3-5: A and b are accumulated as written
+ * and A_k^{-1} is recomputed by Gauss-Jordan elimination with partial
+ * pivoting each time A_k changes; theta_k is then recomputed as A_k^{-1} b_k.
+ * There is no rank-1 identity here: that is the GPU path's business.
+ *
+ * Step order: the reward r_{t-1} of the previous decision arrives with the
+ * next context, so ora_decide first applies Eq. 3-5 to the arm chosen at
+ * t-1 with (x_{t-1}, r_{t-1}), then scores x_t, prunes and picks a_t.
+ * ora_commit then records the decision that was taken (the test harness may
+ * commit another near-tied arm), and ora_flush applies the last pending
+ * update without deciding.
+ *
+ * Non-finite inputs: a non-finite r_{t-1} skips that update; a non-finite
+ * x_t yields action -1 (no decision) and no update next step.  Each such
+ * event increments the instance's bad-input counter.
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORA_MAXD 64
+
+typedef struct {
+    int B, K, d, prune, period, sched;
+    double lambda, alpha0;
+    double *A;              /* [B][K][d][d]  Eq. 3 */
+    double *b;              /* [B][K][d]     Eq. 4 */
+    double *Ainv;           /* [B][K][d][d]  inverse of A */
+    double *theta;          /* [B][K][d]     Eq. 5 */
+    unsigned char *active;  /* [B][K]        current action set */
+    int *nsel;              /* [B][K]        times each arm was updated */
+    double *xprev;          /* [B][d]        context of the last decision */
+    int *aprev;             /* [B]           last decision (-1: none) */
+    int *bad;               /* [B]           non-finite inputs seen */
+    long t;                 /* decisions committed so far */
+    int pending;            /* 1 while the last decision awaits its reward */
+} ora_t;
+
+/* Inverse of the d x d matrix M by Gauss-Jordan elimination on [M | I]
+ * with partial pivoting.  Returns 0, or -1 if M is singular. */
+static int gauss_jordan_inverse(int d, const double *M, double *out)
+{
+    double W[ORA_MAXD][2 * ORA_MAXD];
+    for (int r = 0; r < d; ++r)
+        for (int c = 0; c < d; ++c) {
+            W[r][c] = M[r * d + c];
+            W[r][d + c] = (r == c) ? 1.0 : 0.0;
+        }
+    for (int col = 0; col < d; ++col) {
+        int piv = col;
+        for (int r = col + 1; r < d; ++r)
+            if (fabs(W[r][col]) > fabs(W[piv][col])) piv = r;
+        if (W[piv][col] == 0.0) return -1;
+        if (piv != col)
+            for (int c = 0; c < 2 * d; ++c) {
+                double tmp = W[col][c]; W[col][c] = W[piv][c]; W[piv][c] = tmp;
+            }
+        double p = W[col][col];
+        for (int c = 0; c < 2 * d; ++c) W[col][c] /= p;
+        for (int r = 0; r < d; ++r) {
+            if (r == col) continue;
+            double f = W[r][col];
+            if (f == 0.0) continue;
+            for (int c = 0; c < 2 * d; ++c) W[r][c] -= f * W[col][c];
+        }
+    }
+    for (int r = 0; r < d; ++r)
+        for (int c = 0; c < d; ++c) out[r * d + c] = W[r][d + c];
+    return 0;
+}
+
+static int all_finite(const double *v, int n)
+{
+    for (int i = 0; i < n; ++i)
+        if (!isfinite(v[i])) return 0;
+    return 1;
+}
+
+void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
+                 int prune, int period)
+{
+    if (B < 1 || K < 1 || d < 1 || d > ORA_MAXD || !(lambda > 0.0) || period < 1)
+        return NULL;
+    ora_t *o = (ora_t *)calloc(1, sizeof(ora_t));
+    if (!o) return NULL;
+    o->B = B; o->K = K; o->d = d; o->lambda = lambda; o->alpha0 = alpha0;
+    o->sched = sched; o->prune = prune; o->period = period;
+    size_t nk = (size_t)B * K;
+    o->A = (double *)calloc(nk * d * d, sizeof(double));
+    o->b = (double *)calloc(nk * d, sizeof(double));
+    o->Ainv = (double *)calloc(nk * d * d, sizeof(double));
+    o->theta = (double *)calloc(nk * d, sizeof(double));
+    o->active = (unsigned char *)malloc(nk);
+    o->nsel = (int *)calloc(nk, sizeof(int));
+    o->xprev = (double *)calloc((size_t)B * d, sizeof(double));
+    o->aprev = (int *)malloc((size_t)B * sizeof(int));
+    o->bad = (int *)calloc((size_t)B, sizeof(int));
+    if (!o->A || !o->b || !o->Ainv || !o->theta || !o->active || !o->nsel ||
+        !o->xprev || !o->aprev || !o->bad) {
+        free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
+        free(o->nsel); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+        return NULL;
+    }
+    /* A_k(0) = lambda I, b_k(0) = 0, hence A_k^{-1}(0) = I / lambda, theta_k(0) = 0. */
+    for (size_t k = 0; k < nk; ++k)
+        for (int r = 0; r < d; ++r) {
+            o->A[(k * d + r) * d + r] = lambda;
+            o->Ainv[(k * d + r) * d + r] = 1.0 / lambda;
+        }
+    memset(o->active, 1, nk);
+    for (int i = 0; i < B; ++i) o->aprev[i] = -1;
+    return o;
+}
+
+void ora_destroy(void *h)
+{
+    ora_t *o = (ora_t *)h;
+    if (!o) return;
+    free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
+    free(o->nsel); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+}
+
+/* Eq. 3-5 for arm k of instance i with context x and reward r. */
+static void update_arm(ora_t *o, int i, int k, const double *x, double r)
+{
+    const int d = o->d;
+    size_t ik = (size_t)i * o->K + k;
+    double *A = o->A + ik * d * d, *b = o->b + ik * d;
+    double *Ainv = o->Ainv + ik * d * d, *theta = o->theta + ik * d;
+    for (int p = 0; p < d; ++p)
+        for (int q = 0; q < d; ++q) A[p * d + q] += x[p] * x[q];      /* Eq. 3 */
+    for (int p = 0; p < d; ++p) b[p] += r * x[p];                      /* Eq. 4 */
+    gauss_jordan_inverse(d, A, Ainv);  /* A is lambda I plus PSD terms: never singular */
+    for (int p = 0; p < d; ++p) {                                       /* Eq. 5 */
+        double s = 0.0;
+        for (int q = 0; q < d; ++q) s += Ainv[p * d + q] * b[q];
+        theta[p] = s;
+    }
+    o->nsel[ik] += 1;
+}
+
+static void apply_pending(ora_t *o, int i, const double *r)
+{
+    int a = o->aprev[i];
+    if (a < 0) return;
+    if (r == NULL || !isfinite(r[i])) { o->bad[i] += 1; return; }
+    update_arm(o, i, a, o->xprev + (size_t)i * o->d, r[i]);
+}
+
+double ora_alpha(const void *h, long t)
+{
+    const ora_t *o = (const ora_t *)h;
+    return o->sched == 0 ? o->alpha0 : o->alpha0 / sqrt((double)t + 1.0);
+}
+
+/*
+ * One decision for every instance.
+ *   x      [B][d] context x_t
+ *   r      [B]    reward of the previous decision (may be NULL when none is pending)
+ *   ucb, lcb [B][K] out: scores of the arms active before this step's pruning,
+ *                   -INFINITY for arms already inactive
+ *   keep   [B][K] out: action set after this step's pruning
+ *   action [B]    out: a_t, or -1 when x_t is not finite
+ * The state's action set and last decision are not changed here: see ora_commit.
+ */
+void ora_decide(void *h, const double *x, const double *r, double *ucb, double *lcb,
+                unsigned char *keep, int *action)
+{
+    ora_t *o = (ora_t *)h;
+    const int B = o->B, K = o->K, d = o->d;
+    const long t = o->t;
+    const int pending = o->pending;
+    const double alpha = ora_alpha(o, t);
+    const int prune_now = o->prune && t > 0 && (t % o->period) == 0;
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int i = 0; i < B; ++i) {
+        if (pending) apply_pending(o, i, r);
+        const double *xi = x + (size_t)i * d;
+        const unsigned char *act = o->active + (size_t)i * K;
+        double *U = ucb + (size_t)i * K, *L = lcb + (size_t)i * K;
+        unsigned char *kp = keep + (size_t)i * K;
+        for (int k = 0; k < K; ++k) { U[k] = -INFINITY; L[k] = -INFINITY; kp[k] = act[k]; }
+        if (!all_finite(xi, d)) { o->bad[i] += 1; action[i] = -1; continue; }
+        for (int k = 0; k < K; ++k) {
+            if (!act[k]) continue;
+            size_t ik = (size_t)i * K + k;
+            const double *Ainv = o->Ainv + ik * d * d, *theta = o->theta + ik * d;
+            double m = 0.0, quad = 0.0;
+            for (int p = 0; p < d; ++p) m += theta[p] * xi[p];
+            for (int p = 0; p < d; ++p) {
+                double row = 0.0;
+                for (int q = 0; q < d; ++q) row += Ainv[p * d + q] * xi[q];
+                quad += xi[p] * row;
+            }
+            double w = sqrt(quad > 0.0 ? quad : 0.0);
+            U[k] = m + alpha * w;
+            L[k] = m - alpha * w;
+        }
+        if (prune_now) {
+            double lstar = -INFINITY;
+            for (int k = 0; k < K; ++k)
+                if (act[k] && L[k] > lstar) lstar = L[k];
+            for (int k = 0; k < K; ++k)
+                if (act[k] && U[k] < lstar) kp[k] = 0;
+        }
+        int best = -1;
+        for (int k = 0; k < K; ++k)
+            if (kp[k] && (best < 0 || U[k] > U[best])) best = k;
+        action[i] = best;
+    }
+    o->pending = 0;
+}
+
+/* Record the decision taken at this step: x_t, a_t and the action set. */
+void ora_commit(void *h, const double *x, const int *action, const unsigned char *keep)
+{
+    ora_t *o = (ora_t *)h;
+    const int B = o->B, K = o->K, d = o->d;
+    for (int i = 0; i < B; ++i) {
+        memcpy(o->xprev + (size_t)i * d, x + (size_t)i * d, sizeof(double) * d);
+        o->aprev[i] = action[i];
+        if (keep) memcpy(o->active + (size_t)i * K, keep + (size_t)i * K, K);
+    }
+    o->t += 1;
+    o->pending = 1;
+}
+
+/* Apply the last pending update (rewards of the final decisions). */
+void ora_flush(void *h, const double *r)
+{
+    ora_t *o = (ora_t *)h;
+    if (o->pending)
+        for (int i = 0; i < o->B; ++i) apply_pending(o, i, r);
+    o->pending = 0;
+    for (int i = 0; i < o->B; ++i) o->aprev[i] = -1;
+}
+
+/* Copy out instance i's state; any output pointer may be NULL. */
+void ora_get(const void *h, int i, double *A, double *b, double *Ainv, double *theta,
+             unsigned char *active, int *nsel, int *bad)
+{
+    const ora_t *o = (const ora_t *)h;
+    const int K = o->K, d = o->d;
+    size_t base = (size_t)i * K;
+    if (A) memcpy(A, o->A + base * d * d, sizeof(double) * K * d * d);
+    if (b) memcpy(b, o->b + base * d, sizeof(double) * K * d);
+    if (Ainv) memcpy(Ainv, o->Ainv + base * d * d, sizeof(double) * K * d * d);
+    if (theta) memcpy(theta, o->theta + base * d, sizeof(double) * K * d);
+    if (active) memcpy(active, o->active + base, K);
+    if (nsel) memcpy(nsel, o->nsel + base, sizeof(int) * K);
+    if (bad) *bad = o->bad[i];
+}
+
+long ora_t_now(const void *h) { return ((const ora_t *)h)->t; }
+
+int ora_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void ora_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

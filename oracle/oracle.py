@@ -1,0 +1,140 @@
+"""ctypes front end of the C oracle (agft_oracle.c).
+
+Test infrastructure only: see the header of agft_oracle.c for what is
+computed and which readings of the paper it takes.
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "agft_oracle.c")
+_LIB = os.path.join(_HERE, "libagft_oracle.so")
+_lib = None
+
+
+def build_library(src=_SRC, out=_LIB, extra_flags=()):
+    """Compile the oracle with gcc (fp64, OpenMP over instances)."""
+    cmd = ["gcc", "-O2", "-std=c99", "-fopenmp", "-fPIC", "-shared", "-Wall",
+           *extra_flags, src, "-o", out + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def _declare(lib):
+    P, I, D, L = ctypes.c_void_p, ctypes.c_int, ctypes.c_double, ctypes.c_long
+    lib.ora_create.restype = P
+    lib.ora_create.argtypes = [I, I, I, D, D, I, I, I]
+    lib.ora_destroy.argtypes = [P]
+    lib.ora_decide.argtypes = [P, P, P, P, P, P, P]
+    lib.ora_commit.argtypes = [P, P, P, P]
+    lib.ora_flush.argtypes = [P, P]
+    lib.ora_get.argtypes = [P, I, P, P, P, P, P, P, P]
+    lib.ora_alpha.restype = D
+    lib.ora_alpha.argtypes = [P, L]
+    lib.ora_t_now.restype = L
+    lib.ora_t_now.argtypes = [P]
+    lib.ora_threads.restype = I
+    lib.ora_set_threads.argtypes = [I]
+    return lib
+
+
+def load_library(path=None):
+    """Load the oracle library, building it first if it is not there."""
+    global _lib
+    if path is not None:
+        return _declare(ctypes.CDLL(path))
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build_library()
+        _lib = _declare(ctypes.CDLL(_LIB))
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+class Oracle:
+    """B independent disjoint-LinUCB tuners in double precision (Eq. 1-5)."""
+
+    def __init__(self, B, K, d, lam=1.0, alpha0=1.0, sched=0, prune=0, period=50,
+                 lib=None):
+        self.lib = lib if lib is not None else load_library()
+        self.B, self.K, self.d = int(B), int(K), int(d)
+        self.h = self.lib.ora_create(self.B, self.K, self.d, float(lam), float(alpha0),
+                                     int(sched), int(prune), int(period))
+        if not self.h:
+            raise ValueError("oracle: invalid configuration")
+
+    @classmethod
+    def from_workload(cls, wl, B=None, lib=None):
+        return cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0,
+                   wl.alpha_sched, wl.prune, wl.period, lib=lib)
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h:
+            self.lib.ora_destroy(h)
+            self.h = None
+
+    @property
+    def t(self):
+        return int(self.lib.ora_t_now(self.h))
+
+    def alpha(self, t=None):
+        return float(self.lib.ora_alpha(self.h, self.t if t is None else int(t)))
+
+    def decide(self, x, r=None):
+        """Apply the pending update, score x_t, prune, pick a_t.
+
+        Returns (ucb [B][K], lcb [B][K], keep [B][K] bool, action [B])."""
+        x = np.ascontiguousarray(x, dtype=np.float64).reshape(self.B, self.d)
+        r = None if r is None else np.ascontiguousarray(r, dtype=np.float64).reshape(self.B)
+        ucb = np.empty((self.B, self.K))
+        lcb = np.empty((self.B, self.K))
+        keep = np.empty((self.B, self.K), dtype=np.uint8)
+        action = np.empty(self.B, dtype=np.int32)
+        self.lib.ora_decide(self.h, _ptr(x), _ptr(r), _ptr(ucb), _ptr(lcb), _ptr(keep),
+                            _ptr(action))
+        return ucb, lcb, keep.astype(bool), action
+
+    def commit(self, x, action, keep):
+        x = np.ascontiguousarray(x, dtype=np.float64).reshape(self.B, self.d)
+        action = np.ascontiguousarray(action, dtype=np.int32).reshape(self.B)
+        keep = np.ascontiguousarray(keep, dtype=np.uint8).reshape(self.B, self.K)
+        self.lib.ora_commit(self.h, _ptr(x), _ptr(action), _ptr(keep))
+
+    def step(self, x, r=None):
+        """decide + commit of the oracle's own decision."""
+        ucb, lcb, keep, action = self.decide(x, r)
+        self.commit(x, action, keep)
+        return ucb, lcb, keep, action
+
+    def flush(self, r):
+        r = np.ascontiguousarray(r, dtype=np.float64).reshape(self.B)
+        self.lib.ora_flush(self.h, _ptr(r))
+
+    def get(self, i):
+        K, d = self.K, self.d
+        out = dict(A=np.empty((K, d, d)), b=np.empty((K, d)), Ainv=np.empty((K, d, d)),
+                   theta=np.empty((K, d)), active=np.empty(K, dtype=np.uint8),
+                   nsel=np.empty(K, dtype=np.int32))
+        bad = ctypes.c_int(0)
+        self.lib.ora_get(self.h, int(i), _ptr(out["A"]), _ptr(out["b"]), _ptr(out["Ainv"]),
+                         _ptr(out["theta"]), _ptr(out["active"]), _ptr(out["nsel"]),
+                         ctypes.byref(bad))
+        out["active"] = out["active"].astype(bool)
+        out["bad"] = bad.value
+        return out
+
+    @staticmethod
+    def threads():
+        return int(load_library().ora_threads())
+
+    @staticmethod
+    def set_threads(n):
+        load_library().ora_set_threads(int(n))

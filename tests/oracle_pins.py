@@ -1,0 +1,302 @@
+"""Checks that pin the fp64 oracle to the mathematics rather than to itself.
+
+Each pin_* function takes an oracle library handle (oracle.load_library())
+and raises AssertionError on a mismatch, so the same checks run against the
+real oracle (test_oracle_pins.py) and against deliberately broken copies of
+it (test_oracle_mutants.py).
+
+None of these recomputes the oracle's arithmetic the oracle's way: the
+references are direct inversion of the design matrix rebuilt from the
+history, the Sherman-Morrison closed form of repeated updates, ridge least
+squares, an exact rational hand derivation, explicit loops for argmax and
+pruning, and statistical convergence on a known linear reward.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+
+from oracle import Oracle
+
+
+def _rand_contexts(rng, T, B, d):
+    x = rng.standard_normal((T, B, d))
+    x[:, :, 0] = 1.0
+    return x
+
+
+def _brute_scores(hist, lam, d, x, alpha):
+    """Scores of one arm from its history via direct inversion / solve."""
+    A = lam * np.eye(d)
+    b = np.zeros(d)
+    for xs, rs in hist:
+        A += np.outer(xs, xs)
+        b += rs * xs
+    theta = np.linalg.solve(A, b)
+    quad = float(x @ np.linalg.solve(A, x))
+    w = math.sqrt(max(0.0, quad))
+    return A, b, theta, theta @ x + alpha * w, theta @ x - alpha * w
+
+
+def _brute_trajectory(lib, B, K, d, T, lam, alpha0, sched, prune, period, seed):
+    """Drive the oracle with random contexts and rewards and check every
+    decision against brute force (explicit history, np.linalg, plain loops)."""
+    rng = np.random.default_rng(seed)
+    xs = _rand_contexts(rng, T, B, d)
+    rs = rng.uniform(-2.0, 0.0, size=(T, B))
+    ora = Oracle(B, K, d, lam, alpha0, sched, prune, period, lib=lib)
+    hist = [[[] for _ in range(K)] for _ in range(B)]
+    active = np.ones((B, K), dtype=bool)
+    r_prev = None
+    for t in range(T):
+        ucb, lcb, keep, action = ora.decide(xs[t], r_prev)
+        alpha = alpha0 if sched == 0 else alpha0 / math.sqrt(t + 1.0)
+        for i in range(B):
+            U = np.full(K, -np.inf)
+            L = np.full(K, -np.inf)
+            for k in range(K):
+                if active[i, k]:
+                    _, _, _, U[k], L[k] = _brute_scores(hist[i][k], lam, d, xs[t, i], alpha)
+            for k in range(K):
+                if active[i, k]:
+                    assert abs(ucb[i, k] - U[k]) <= 1e-9 * max(1.0, abs(U[k])), (t, i, k)
+                    assert abs(lcb[i, k] - L[k]) <= 1e-9 * max(1.0, abs(L[k])), (t, i, k)
+                else:
+                    assert ucb[i, k] == -np.inf
+            new_active = active[i].copy()
+            if prune and t > 0 and t % period == 0:
+                lstar = max(L[k] for k in range(K) if active[i, k])
+                for k in range(K):
+                    if active[i, k] and U[k] < lstar:
+                        new_active[k] = False
+            assert (keep[i] == new_active).all(), (t, i)
+            best = -1
+            for k in range(K):
+                if new_active[k] and (best < 0 or U[k] > U[best]):
+                    best = k
+            assert action[i] == best, (t, i, action[i], best)
+            active[i] = new_active
+            hist[i][best].append((xs[t, i], rs[t, i]))
+        ora.commit(xs[t], action, keep)
+        r_prev = rs[t]
+    ora.flush(r_prev)
+    for i in range(B):
+        st = ora.get(i)
+        for k in range(K):
+            A, b, theta, _, _ = _brute_scores(hist[i][k], lam, d, xs[0, i], 0.0)
+            assert np.allclose(st["A"][k], A, rtol=1e-12, atol=1e-12)
+            assert np.allclose(st["b"][k], b, rtol=1e-12, atol=1e-12)
+            Ainv = np.linalg.inv(A)
+            assert np.abs(st["Ainv"][k] - Ainv).max() <= 1e-10 * np.abs(Ainv).max()
+            assert np.abs(st["theta"][k] - theta).max() <= 1e-10 * max(1.0, np.abs(theta).max())
+            assert st["nsel"][k] == len(hist[i][k])
+        assert (st["active"] == active[i]).all()
+
+
+def pin_brute_force_small(lib):
+    """Direct inversion + explicit argmax/prune loops on tiny random cases."""
+    _brute_trajectory(lib, B=2, K=3, d=1, T=30, lam=1.0, alpha0=1.0, sched=0, prune=0,
+                      period=5, seed=1)
+    _brute_trajectory(lib, B=2, K=4, d=2, T=40, lam=0.5, alpha0=0.7, sched=1, prune=1,
+                      period=7, seed=2)
+    _brute_trajectory(lib, B=3, K=4, d=4, T=48, lam=2.0, alpha0=0.5, sched=0, prune=1,
+                      period=5, seed=3)
+    _brute_trajectory(lib, B=1, K=4, d=8, T=64, lam=1.0, alpha0=0.3, sched=0, prune=1,
+                      period=4, seed=4)
+
+
+def pin_repeated_update_closed_form(lib):
+    """n identical updates with x: the Sherman-Morrison closed form.
+
+    A = lam I + n x x^T  =>  A^{-1} = (I - n x x^T / (lam + n |x|^2)) / lam,
+    x^T A^{-1} x = |x|^2 / (lam + n |x|^2),  theta = (sum r) x / (lam + n |x|^2).
+    """
+    d, lam, n = 5, 1.7, 37
+    x = np.array([1.0, -0.5, 2.0, 0.25, -1.5])
+    rng = np.random.default_rng(5)
+    rs = rng.normal(size=n)
+    ora = Oracle(1, 1, d, lam, 0.8, 0, 0, 50, lib=lib)
+    r_prev = None
+    for s in range(n):
+        ucb, lcb, keep, action = ora.step(x[None, :], r_prev)
+        assert action[0] == 0
+        r_prev = rs[s:s + 1]
+    ucb, lcb, keep, action = ora.decide(x[None, :], r_prev)
+    nx2 = float(x @ x)
+    denom = lam + n * nx2
+    Ainv = (np.eye(d) - n * np.outer(x, x) / denom) / lam
+    theta = rs.sum() * x / denom
+    st = ora.get(0)
+    assert np.abs(st["Ainv"][0] - Ainv).max() <= 1e-12
+    assert np.abs(st["theta"][0] - theta).max() <= 1e-12
+    w = math.sqrt(nx2 / denom)
+    m = rs.sum() * nx2 / denom
+    assert abs(ucb[0, 0] - (m + 0.8 * w)) <= 1e-12
+    assert abs(lcb[0, 0] - (m - 0.8 * w)) <= 1e-12
+
+
+def pin_ridge_least_squares(lib):
+    """K = 1: theta is the ridge solution of the observed (x, r) pairs (Eq. 5)."""
+    d, lam, T = 6, 0.3, 80
+    rng = np.random.default_rng(6)
+    xs = _rand_contexts(rng, T, 1, d)[:, 0]
+    rs = rng.normal(size=T)
+    ora = Oracle(1, 1, d, lam, 0.0, 0, 0, 50, lib=lib)
+    r_prev = None
+    for t in range(T):
+        ora.step(xs[t][None, :], r_prev)
+        r_prev = rs[t:t + 1]
+    ora.flush(r_prev)
+    Xa = np.vstack([xs, math.sqrt(lam) * np.eye(d)])
+    ya = np.concatenate([rs, np.zeros(d)])
+    theta_ls = np.linalg.lstsq(Xa, ya, rcond=None)[0]
+    assert np.abs(ora.get(0)["theta"][0] - theta_ls).max() <= 1e-10
+
+
+def pin_rational_worked_example(lib):
+    """Hand-worked d = 2, K = 2 trajectory in exact rational arithmetic."""
+    from golden_example import load_worked_example
+    ex = load_worked_example()
+    d, K = 2, 2
+    lam, alpha = ex["lambda"], ex["alpha"]
+    ora = Oracle(1, K, d, float(lam), float(alpha), 0, 0, 50, lib=lib)
+    r_prev = None
+    for step in ex["steps"]:
+        x = np.array([float(v) for v in step["x"]])
+        ucb, lcb, keep, action = ora.step(x[None, :], r_prev)
+        assert action[0] == step["action"], (step, action)
+        for k in range(K):
+            m, q = step["mean"][k], step["quad"][k]
+            expect = float(m) + float(alpha) * math.sqrt(float(q))
+            assert abs(ucb[0, k] - expect) <= 1e-13, (step, k, ucb[0, k], expect)
+        r_prev = np.array([float(step["reward"])])
+    ora.flush(r_prev)
+    st = ora.get(0)
+    for k, (Ainv, theta) in enumerate(zip(ex["final_Ainv"], ex["final_theta"])):
+        assert np.abs(st["Ainv"][k] - np.array(Ainv, dtype=float)).max() <= 1e-14
+        assert np.abs(st["theta"][k] - np.array(theta, dtype=float)).max() <= 1e-14
+
+
+def pin_textbook_reductions(lib):
+    """K = 1 always picks arm 0; untouched arms tie and are swept in index
+    order; alpha = 0 is greedy on theta^T x; d = 1 is the scalar formula."""
+    rng = np.random.default_rng(7)
+    ora = Oracle(2, 1, 3, 1.0, 1.0, 0, 1, 5, lib=lib)
+    r_prev = None
+    for t in range(20):
+        x = _rand_contexts(rng, 1, 2, 3)[0]
+        _, _, _, action = ora.step(x, r_prev)
+        assert (action == 0).all()
+        r_prev = rng.normal(size=2)
+    K = 6
+    ora = Oracle(1, K, 4, 1.0, 1.0, 0, 0, 50, lib=lib)
+    r_prev = None
+    seen = []
+    x = _rand_contexts(rng, 1, 1, 4)[0]
+    for t in range(K):
+        # a touched arm now has mean r |x|^2/(lam+|x|^2) < 0 and a smaller width
+        ucb, _, _, action = ora.step(x, r_prev)
+        seen.append(int(action[0]))
+        r_prev = np.array([-1.0])
+    assert seen == list(range(K))
+    ora = Oracle(1, 3, 2, 1.0, 0.0, 0, 0, 50, lib=lib)
+    hist = [[] for _ in range(3)]
+    r_prev = None
+    for t in range(30):
+        x = np.array([1.0, rng.normal()])
+        ucb, _, _, action = ora.step(x[None, :], r_prev)
+        greedy = []
+        for k in range(3):
+            A = np.eye(2) + sum((np.outer(a, a) for a, _ in hist[k]), np.zeros((2, 2)))
+            b = sum((r * a for a, r in hist[k]), np.zeros(2))
+            greedy.append(np.linalg.solve(A, b) @ x)
+        best = max(range(3), key=lambda k: (greedy[k], -k))
+        assert action[0] == best
+        r = float(rng.normal() - 0.3 * best)
+        hist[best].append((x, r))
+        r_prev = np.array([r])
+    lam, alpha = 2.0, 0.6
+    ora = Oracle(1, 2, 1, lam, alpha, 0, 0, 50, lib=lib)
+    sums = [[lam, 0.0], [lam, 0.0]]   # per arm: lam + sum x^2, sum r x
+    r_prev = None
+    for t in range(25):
+        x = float(rng.uniform(0.5, 2.0))
+        ucb, _, _, action = ora.step(np.array([[x]]), r_prev)
+        for k in range(2):
+            a, s = sums[k]
+            assert abs(ucb[0, k] - (s / a * x + alpha * abs(x) / math.sqrt(a))) <= 1e-12
+        r = float(rng.normal())
+        sums[action[0]][0] += x * x
+        sums[action[0]][1] += r * x
+        r_prev = np.array([r])
+
+
+def pin_prune_invariants(lib):
+    """Along random trajectories with pruning: the action set only shrinks,
+    the arms with the largest UCB and the largest LCB always survive, so the
+    set is never empty; with alpha = 0 one prune leaves only the arms whose
+    estimate ties the best."""
+    rng = np.random.default_rng(8)
+    B, K, d, T = 4, 12, 4, 120
+    ora = Oracle(B, K, d, 1.0, 0.4, 0, 1, 10, lib=lib)
+    prev = np.ones((B, K), dtype=bool)
+    r_prev = None
+    for t in range(T):
+        x = _rand_contexts(rng, 1, B, d)[0]
+        ucb, lcb, keep, action = ora.step(x, r_prev)
+        assert not (keep & ~prev).any()
+        assert keep.any(axis=1).all()
+        if t > 0 and t % 10 == 0:
+            for i in range(B):
+                act = np.flatnonzero(prev[i])
+                assert keep[i, act[np.argmax(ucb[i, act])]]
+                assert keep[i, act[np.argmax(lcb[i, act])]]
+        prev = keep
+        r_prev = rng.normal(size=B) - 0.1 * action
+    ora = Oracle(1, 5, 2, 1.0, 0.0, 0, 1, 6, lib=lib)
+    r_prev = None
+    for t in range(7):
+        x = np.array([[1.0, 0.5]])
+        ucb, lcb, keep, action = ora.step(x, r_prev)
+        r_prev = np.array([-1.0 - 0.1 * t])
+    # alpha = 0: UCB = LCB = theta^T x, so the prune at t = 6 keeps exactly
+    # the arms whose estimate equals the maximum
+    m = ucb[0]
+    assert keep[0].sum() == (m == m.max()).sum()
+    assert keep[0, int(np.argmax(m))]
+
+
+def pin_convergence_linear_reward(lib):
+    """Linear rewards r = theta*_k^T x + N(0, s^2): the estimates converge at
+    the statistical rate and the tuner settles on the best arm."""
+    rng = np.random.default_rng(9)
+    K, d, T, s = 3, 4, 6000, 0.1
+    theta_star = np.array([[0.0, 0.5, -0.3, 0.2],
+                           [0.4, 0.5, -0.3, 0.2],
+                           [0.1, -0.2, 0.3, 0.0]])
+    ora = Oracle(1, K, d, 1.0, 0.5, 0, 0, 50, lib=lib)
+    r_prev = None
+    best_count = 0
+    regret = np.zeros(T)
+    for t in range(T):
+        x = np.concatenate([[1.0], rng.standard_normal(d - 1)])
+        _, _, _, action = ora.step(x[None, :], r_prev)
+        a = int(action[0])
+        means = theta_star @ x
+        regret[t] = means.max() - means[a]
+        if t >= T - 1000 and a == int(np.argmax(means)):
+            best_count += 1
+        r_prev = np.array([means[a] + s * rng.standard_normal()])
+    ora.flush(r_prev)
+    st = ora.get(0)
+    n1 = st["nsel"][1]
+    err = np.linalg.norm(st["theta"][1] - theta_star[1])
+    assert n1 > T // 2
+    assert err <= 5 * s * math.sqrt(d / n1) + np.linalg.norm(theta_star[1]) / n1
+    assert best_count >= 900
+    assert regret[T // 2:].sum() < regret[:T // 2].sum()
+
+
+ALL_PINS = [pin_brute_force_small, pin_repeated_update_closed_form, pin_ridge_least_squares,
+            pin_rational_worked_example, pin_textbook_reductions, pin_prune_invariants,
+            pin_convergence_linear_reward]

@@ -1,0 +1,61 @@
+"""Plant plausible mistakes in a copy of the oracle (CPU only) and check that
+the pins catch every one.  The planted copies are compiled into a temporary
+directory; the real oracle is untouched."""
+import os
+
+import pytest
+
+import oracle_pins as pins
+from oracle import build_library, load_library
+from oracle.oracle import _SRC
+
+# Pruning at t = 0 as well is not listed: every arm is still in its initial
+# state then, all scores tie, and the prune cannot remove anything, so that
+# change is equivalent rather than a mistake.
+MUTANTS = {
+    "eq3_dropped_outer_product": ("A[p * d + q] += x[p] * x[q];", "A[p * d + q] += x[p] * x[p];"),
+    "eq4_wrong_sign": ("b[p] += r * x[p];", "b[p] -= r * x[p];"),
+    "eq5_transposed_index": ("s += Ainv[p * d + q] * b[q];", "s += Ainv[p * d + q] * b[p];"),
+    "score_wrong_operand": ("row += Ainv[p * d + q] * xi[q];", "row += Ainv[p * d + q] * xi[p];"),
+    "lcb_wrong_sign": ("L[k] = m - alpha * w;", "L[k] = m + alpha * w;"),
+    "ties_to_highest_index": ("(best < 0 || U[k] > U[best])", "(best < 0 || U[k] >= U[best])"),
+    "prune_non_strict": ("if (act[k] && U[k] < lstar) kp[k] = 0;",
+                         "if (act[k] && U[k] <= lstar) kp[k] = 0;"),
+    "prune_period_off_by_one": ("(t % o->period) == 0", "((t + 1) % o->period) == 0"),
+    "alpha_schedule_no_plus_one": ("sqrt((double)t + 1.0)", "sqrt((double)t + 2.0)"),
+    "init_inverse_not_scaled": ("o->Ainv[(k * d + r) * d + r] = 1.0 / lambda;",
+                                "o->Ainv[(k * d + r) * d + r] = lambda;"),
+    "gauss_jordan_sign": ("W[r][c] -= f * W[col][c];", "W[r][c] += f * W[col][c];"),
+    "update_wrong_arm": ("update_arm(o, i, a, o->xprev", "update_arm(o, i, (a + 1) % o->K, o->xprev"),
+    "update_uses_current_context": ("update_arm(o, i, a, o->xprev + (size_t)i * o->d, r[i]);",
+                                    "update_arm(o, i, a, o->xprev, r[i]);"),
+    "width_without_root": ("double w = sqrt(quad > 0.0 ? quad : 0.0);",
+                           "double w = quad > 0.0 ? quad : 0.0;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(_SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    mutant_src = tmp_path / "mutant.c"
+    mutant_src.write_text(src.replace(old, new))
+    lib_path = build_library(str(mutant_src), str(tmp_path / "libmutant.so"))
+    lib = load_library(lib_path)
+    caught = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(lib)
+        except AssertionError:
+            caught.append(pin.__name__)
+        except (ValueError, FloatingPointError, ZeroDivisionError, IndexError):
+            caught.append(pin.__name__)
+    assert caught, f"mutant {name} survived every pin"
+
+
+def test_unmutated_copy_passes(tmp_path):
+    lib_path = build_library(_SRC, str(tmp_path / "libcopy.so"))
+    lib = load_library(lib_path)
+    for pin in pins.ALL_PINS:
+        pin(lib)
