@@ -1,0 +1,151 @@
+/*
+ * agft.h -- C ABI of the batched AGFT tuner step on AMD Instinct MI355X (gfx950).
+ *
+ * One call of agft_step advances B independent tuner instances by one
+ * decision of AGFT's contextual-bandit frequency selector (Sec. 4.2): it
+ * folds the previous decision's reward into that arm's model (Eq. 3-5),
+ * scores every active frequency arm on the new context with the linear upper
+ * confidence bound (Eq. 1), applies the action-space pruning rule when due
+ * (motivated in Sec. 4.3), and returns the argmax arm per instance.
+ *
+ * Memory: the caller owns every device buffer (state, contexts, rewards,
+ * actions, score dumps); the library owns only the small host-side handle.
+ * No entry point allocates or frees device memory.  Every entry point only
+ * enqueues work on the handle's HIP stream and returns without waiting,
+ * except agft_create with AGFT_ADOPT_STATE, which reads the buffer's header
+ * back synchronously.  A handle is not thread-safe; use one handle per
+ * stream.
+ *
+ * Errors: every int-returning call returns AGFT_OK (0) or a negative code;
+ * arguments are validated before anything is enqueued.  A device fault of
+ * earlier work surfaces as AGFT_E_HIP from a later call.
+ *
+ * Model kept per (instance i, arm k), in fp32:
+ *   theta_k = A_k^{-1} b_k                      (Eq. 5)
+ *   S_k     upper triangular with S_k S_k^T = A_k^{-1}
+ * where A_k = lambda I + sum x x^T (Eq. 3) and b_k = sum r x (Eq. 4) over
+ * the decisions that chose arm k.  The rank-1 change of A_k^{-1} that Eq. 3
+ * implies (the Sherman-Morrison identity) is applied to the factor S_k in
+ * square-root form, which keeps fp32 scores within 1e-5 of exact arithmetic
+ * where the plain inverse update drifts by 1e-3 over thousands of updates.
+ */
+#ifndef AGFT_H
+#define AGFT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define AGFT_ABI_VERSION 1
+
+enum agft_status {
+    AGFT_OK = 0,
+    AGFT_E_INVAL = -1,       /* NULL pointer, size or value out of range */
+    AGFT_E_UNSUPPORTED = -2, /* well-formed but not supported (d not in {8,16,32}) */
+    AGFT_E_STATE = -3,       /* call not valid now (missing reward, adopted
+                                buffer that does not match the configuration) */
+    AGFT_E_HIP = -4          /* HIP runtime error, including earlier device faults */
+};
+
+/* agft_config.flags */
+#define AGFT_ADOPT_STATE 0x1u /* resume from the state already in the buffer */
+
+typedef struct agft_config {
+    int32_t B;            /* independent tuner instances, >= 1 */
+    int32_t K;            /* frequency arms per instance (the set F of Eq. 1), 1..1024 */
+    int32_t d;            /* context features per decision (x_t, Sec. 4.1): 8, 16 or 32 */
+    float lambda;         /* ridge prior, A_k(0) = lambda I: finite, > 0 */
+    float alpha0;         /* exploration weight of Eq. 1: finite, >= 0 */
+    int32_t alpha_sched;  /* 0: alpha_t = alpha0; 1: alpha_t = alpha0 / sqrt(t + 1) */
+    int32_t prune_rule;   /* 0: none; 1: at a pruning step an active arm k is
+                             removed for good when UCB_k < max_j LCB_j over the
+                             active arms j, with that step's context and alpha_t,
+                             before the argmax */
+    int32_t prune_period; /* pruning steps are t > 0 with t % prune_period == 0; >= 1 */
+    uint32_t flags;       /* 0 or AGFT_ADOPT_STATE */
+} agft_config;
+
+typedef struct agft_handle agft_handle;
+
+/* Device pointers into the state buffer and the handle's counters. */
+typedef struct agft_state_view {
+    int64_t t;          /* decisions made so far */
+    int32_t pending;    /* 1 while the last decision awaits its reward */
+    int32_t B, K, d;
+    int32_t chunks;     /* float4 chunks per arm record: d/4 + d(d+1)/8 */
+    int32_t mask_words; /* uint32 words per instance in the action-set mask: ceil(K/32) */
+    void *arms;         /* float4 [B][chunks][K]: chunk c of arm k of instance i at
+                           index (i*chunks + c)*K + k.  A record is theta_0..theta_{d-1}
+                           followed by S packed by columns, upper part only:
+                           S_00, S_01, S_11, S_02, S_12, S_22, ... */
+    uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k active */
+    float *xprev;       /* [B][d]: context of the last decision */
+    int32_t *aprev;     /* [B]: last decision, -1 when there is none */
+    int32_t *kact;      /* [B]: number of active arms */
+    int32_t *nsel;      /* [B][K]: updates applied to each arm */
+    int32_t *bad;       /* [B]: non-finite contexts or rewards met */
+} agft_state_view;
+
+/* Bytes of device state for cfg (a 256-byte header, then the regions listed
+ * in agft_state_view, each 256-byte aligned); 0 if cfg is invalid. */
+size_t agft_state_bytes(const agft_config *cfg);
+
+/*
+ * Bind a handle to the caller's state buffer d_state (nbytes >= agft_state_bytes,
+ * 256-byte aligned) and HIP stream (a hipStream_t; NULL = the null stream).
+ * Without AGFT_ADOPT_STATE, enqueues the initialisation: S_k = I / sqrt(lambda),
+ * theta_k = 0, every arm active, t = 0.  With it, reads the buffer's header
+ * back (synchronously) and resumes from its t; the header must match cfg.
+ * *out receives the handle; on error *out is set to NULL.
+ */
+int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stream,
+                agft_handle **out);
+
+/*
+ * One decision for all B instances (Sec. 4.2):
+ *   1. if a decision is pending, fold its reward d_reward[i] into the chosen
+ *      arm with the stored context (Eq. 3-5; a non-finite reward skips this);
+ *   2. score every active arm on d_ctx (Eq. 1): UCB and LCB;
+ *   3. at pruning steps, apply the pruning rule;
+ *   4. d_action[i] = lowest-index active arm with the largest UCB (-1 when
+ *      the context holds a non-finite value: no decision, no update next step);
+ *   5. remember d_ctx and the action for the next call; t += 1.
+ * d_ctx     [B][d] fp32, device.  NULL = flush: apply step 1 only, no decision.
+ * d_reward  [B] fp32, device: reward of the previous decision; must be non-NULL
+ *           when a decision is pending (AGFT_E_STATE otherwise), else ignored.
+ * d_action  [B] int32, device, or NULL.
+ * d_scores  [B][2][K] fp32, device, or NULL: UCB (row 0) and LCB (row 1) of
+ *           every arm active before this step's pruning, -inf for the others.
+ */
+int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t *d_action,
+              float *d_scores);
+
+/* Fill *out with device pointers into the state and the handle's counters. */
+int agft_get_state(const agft_handle *h, agft_state_view *out);
+
+/*
+ * Materialise the model for inspection: d_theta [B][K][d] = theta_k (Eq. 5)
+ * and d_ainv [B][K][d][d] = A_k^{-1} = S_k S_k^T.  Either may be NULL.
+ */
+int agft_export(agft_handle *h, float *d_theta, float *d_ainv);
+
+/* Enqueue later work of this handle on another HIP stream. */
+int agft_set_stream(agft_handle *h, void *stream);
+
+/* Release the host handle (the state buffer stays the caller's). NULL is a no-op. */
+int agft_destroy(agft_handle *h);
+
+/* Static text for a status code. */
+const char *agft_strerror(int code);
+
+/* AGFT_ABI_VERSION of the loaded library. */
+int agft_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AGFT_H */

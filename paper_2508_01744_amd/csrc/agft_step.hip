@@ -1,0 +1,708 @@
+// agft_step.hip -- batched AGFT decide-and-update step for CDNA4 (gfx950).
+//
+// One workgroup per tuner instance, one lane per frequency arm: lane k of the
+// workgroup streams arm k's record (theta_k and the packed factor S_k of
+// A_k^{-1}) from HBM and scores it without any cross-lane traffic, because
+// the context x_t is uniform over the workgroup and lives in scalar
+// registers.  Records are interleaved across arms in 16-byte chunks, so for
+// every chunk index the 64 lanes of a wavefront read 1 KiB of contiguous
+// memory.
+//
+// Per step and instance (Sec. 4.2):
+//   phase 1  fold the previous decision's reward into its arm: Eq. 3-5 as a
+//            square-root rank-1 update of S (below) plus the matching theta
+//            update, staged in LDS, written back, and the updated arm scored
+//            on x_t from LDS;
+//   phase 2  every other active arm: v = S^T x_t, w^2 = |v|^2, m = theta^T x_t,
+//            UCB = m + alpha_t w, LCB = m - alpha_t w  (Eq. 1);
+//   phase 3  pruning when due (drop UCB_k < max_j LCB_j), argmax with ties to
+//            the lowest arm index, epilogue.
+//
+// Square-root update.  Eq. 3 adds x x^T to A, so P = A^{-1} changes by the
+// Sherman-Morrison identity P' = P - P x x^T P / (1 + x^T P x).  With P = S S^T
+// (S upper triangular) and f = S^T x, P' = S M M^T S^T where M is the upper
+// triangular factor of I - f f^T / alpha_d, alpha_j = 1 + f_0^2 + ... + f_j^2
+// (alpha_{-1} = 1):
+//   M_jj = sqrt(alpha_{j-1} / alpha_j),  M_ij = -f_i f_j / sqrt(alpha_{j-1} alpha_j), i < j,
+// so S' = S M column by column:
+//   S'_ij = M_jj S_ij - f_j / sqrt(alpha_{j-1} alpha_j) * sum_{i<=k<j} f_k S_ik.
+// Eq. 4-5 combine into theta' = theta + g (r - x^T theta) with the gain
+// g = P x / (1 + x^T P x) = S f / alpha_{d-1}.
+// This is the triangular square-root covariance update of sequential
+// estimation (Carlson's form); its fp32 error grows with the square root of
+// the condition number of A rather than with the condition number itself.
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "agft.h"
+
+namespace {
+
+constexpr uint32_t kMagic = 0x54464741u;  // "AGFT"
+constexpr int kWave = 64;
+constexpr int kMaxK = 1024;
+constexpr int kMaxWaves = kMaxK / kWave;
+constexpr size_t kAlign = 256;
+
+// Header at the start of the state buffer (256 bytes).
+struct alignas(16) StateHeader {
+    uint32_t magic;
+    uint32_t version;
+    int32_t B, K, d, chunks, mask_words, pending;
+    int64_t t;
+    float lambda, alpha0;
+    int32_t alpha_sched, prune_rule, prune_period;
+    uint32_t reserved[47];
+};
+static_assert(sizeof(StateHeader) == 256, "header is 256 bytes");
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+int chunks_for(int d) { return d / 4 + d * (d + 1) / 8; }
+
+struct Layout {
+    size_t arms, mask, xprev, aprev, kact, nsel, bad, total;
+};
+
+Layout layout_for(int B, int K, int d) {
+    Layout L;
+    const size_t b = (size_t)B, k = (size_t)K;
+    const size_t kw = (k + 31) / 32;
+    size_t off = sizeof(StateHeader);
+    L.arms = off;  off = align_up(off + b * (size_t)chunks_for(d) * k * 16);
+    L.mask = off;  off = align_up(off + b * kw * 4);
+    L.xprev = off; off = align_up(off + b * (size_t)d * 4);
+    L.aprev = off; off = align_up(off + b * 4);
+    L.kact = off;  off = align_up(off + b * 4);
+    L.nsel = off;  off = align_up(off + b * k * 4);
+    L.bad = off;   off = align_up(off + b * 4);
+    L.total = off;
+    return L;
+}
+
+// Record geometry for context dimension D.
+template <int D>
+struct Rec {
+    static constexpr int NT = D / 4;             // theta chunks
+    static constexpr int NSE = D * (D + 1) / 2;  // packed factor elements
+    static constexpr int NS = NSE / 4;           // factor chunks
+    static constexpr int C = NT + NS;            // chunks per record
+    static constexpr int F = 4 * C;              // floats per record
+    static_assert(NSE % 4 == 0, "packed factor fills whole chunks");
+};
+
+// Packed column-major index of S_ij (i <= j) within the factor part.
+__host__ __device__ constexpr int packed(int i, int j) { return j * (j + 1) / 2 + i; }
+
+// Column j and row i of packed element e.
+__device__ inline void unpack(int e, int &i, int &j) {
+    int c = 0;
+    while ((c + 1) * (c + 2) / 2 <= e) ++c;
+    j = c;
+    i = e - c * (c + 1) / 2;
+}
+
+// Eq. 1 ingredients of one arm record: m = theta^T x and w2 = |S^T x|^2.
+// get(c) yields chunk c of the record; the operation order is fixed so the
+// streaming path and the LDS path give bit-identical results on equal data.
+template <int D, class Get>
+__device__ __forceinline__ void score_record(Get get, const float *x, float &m, float &w2) {
+    m = 0.0f;
+#pragma unroll
+    for (int c = 0; c < Rec<D>::NT; ++c) {
+        const float4 v = get(c);
+        m = fmaf(v.x, x[4 * c + 0], m);
+        m = fmaf(v.y, x[4 * c + 1], m);
+        m = fmaf(v.z, x[4 * c + 2], m);
+        m = fmaf(v.w, x[4 * c + 3], m);
+    }
+    w2 = 0.0f;
+    float acc = 0.0f;
+    int i = 0, j = 0;
+#pragma unroll
+    for (int c = 0; c < Rec<D>::NS; ++c) {
+        const float4 v = get(Rec<D>::NT + c);
+        const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc = fmaf(e[q], x[i], i == 0 ? 0.0f : acc);
+            if (i == j) {
+                w2 = fmaf(acc, acc, w2);
+                ++j;
+                i = 0;
+            } else {
+                ++i;
+            }
+        }
+    }
+}
+
+struct StepArgs {
+    float4 *arms;
+    uint32_t *mask;
+    float *xprev;
+    int32_t *aprev;
+    int32_t *kact;
+    int32_t *nsel;
+    int32_t *bad;
+    StateHeader *hdr;
+    const float *ctx;     // [B][D] or nullptr (flush)
+    const float *reward;  // [B] or nullptr
+    int32_t *action;      // [B] or nullptr
+    float *scores;        // [B][2][K] or nullptr
+    int32_t B, K, KW;
+    int32_t apply_update;  // a decision is pending
+    int32_t prune_now;
+    float alpha;
+    int64_t t_next;        // t after this call (header bookkeeping)
+};
+
+struct BestPair {
+    float v;
+    int k;
+};
+
+__device__ inline BestPair better(BestPair a, BestPair b) {
+    if (b.v > a.v || (b.v == a.v && b.k < a.k)) return b;
+    return a;
+}
+
+template <int D>
+__global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
+    using R = Rec<D>;
+    const int inst = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int nthr = blockDim.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    const int nwave = nthr / kWave;
+    const int K = p.K;
+    const size_t rec_base = (size_t)inst * R::C * (size_t)K;
+
+    __shared__ float4 s_old[R::C];
+    __shared__ float4 s_new[R::C];
+    __shared__ float s_xp[D];
+    __shared__ float s_x[D];
+    __shared__ float s_f[D];
+    __shared__ float s_ca[D];
+    __shared__ float s_cb[D];
+    __shared__ float s_scal[4];   // alpha_{d-1}, prediction error, m_a, w2_a
+    __shared__ float s_v[D];
+    __shared__ float s_red_v[kMaxWaves];
+    __shared__ int s_red_k[kMaxWaves];
+    __shared__ int s_red_n[kMaxWaves];
+
+    const bool decide = p.ctx != nullptr;
+
+    // Context of this decision: uniform across the workgroup.
+    float x[D];
+    bool x_ok = true;
+    if (decide) {
+        const float *xi = p.ctx + (size_t)inst * D;
+#pragma unroll
+        for (int q = 0; q < D; ++q) {
+            x[q] = xi[q];
+            x_ok = x_ok && isfinite(x[q]);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < D; ++q) x[q] = 0.0f;
+    }
+
+    // ---- phase 1: pending update of the previous decision's arm ----
+    const int a_prev = p.apply_update ? p.aprev[inst] : -1;
+    int a_upd = -1;
+    if (a_prev >= 0 && a_prev < K) {
+        const float r = p.reward[inst];
+        if (isfinite(r)) {
+            a_upd = a_prev;
+            for (int c = tid; c < R::C; c += nthr) s_old[c] = p.arms[rec_base + (size_t)c * K + a_upd];
+            if (tid < D) s_xp[tid] = p.xprev[(size_t)inst * D + tid];
+            if (tid < D) s_x[tid] = x[tid];
+            __syncthreads();
+            const float *so = reinterpret_cast<const float *>(s_old);
+            const float *sth = so;             // theta
+            const float *sS = so + D;          // packed factor
+            if (tid < D) {
+                // f_j = sum_{i<=j} S_ij xp_i
+                const int j = tid;
+                float acc = 0.0f;
+                for (int i = 0; i <= j; ++i) acc = fmaf(sS[packed(i, j)], s_xp[i], acc);
+                s_f[j] = acc;
+            }
+            __syncthreads();
+            if (tid == 0) {
+                float al = 1.0f;
+                for (int j = 0; j < D; ++j) {
+                    const float an = fmaf(s_f[j], s_f[j], al);
+                    s_ca[j] = sqrtf(al / an);
+                    s_cb[j] = s_f[j] / sqrtf(al * an);
+                    al = an;
+                }
+                float pred = 0.0f;
+                for (int i = 0; i < D; ++i) pred = fmaf(s_xp[i], sth[i], pred);
+                s_scal[0] = al;
+                s_scal[1] = r - pred;
+            }
+            __syncthreads();
+            float *sn = reinterpret_cast<float *>(s_new);
+            for (int e = tid; e < R::NSE; e += nthr) {
+                int i, j;
+                unpack(e, i, j);
+                float g = 0.0f;
+                for (int k = i; k < j; ++k) g = fmaf(s_f[k], sS[packed(i, k)], g);
+                sn[D + e] = s_ca[j] * sS[e] - s_cb[j] * g;
+            }
+            if (tid < D) {
+                // gain g_i = (S f)_i / alpha_{d-1}
+                const int i = tid;
+                float sf = 0.0f;
+                for (int k = i; k < D; ++k) sf = fmaf(sS[packed(i, k)], s_f[k], sf);
+                sn[i] = fmaf(sf / s_scal[0], s_scal[1], sth[i]);
+            }
+            __syncthreads();
+            for (int c = tid; c < R::C; c += nthr) p.arms[rec_base + (size_t)c * K + a_upd] = s_new[c];
+            if (tid == 0) p.nsel[(size_t)inst * K + a_upd] += 1;
+            // score the updated arm on x_t from LDS, in the streaming path's order
+            if (decide && x_ok) {
+                if (tid < D) {
+                    const int j = tid;
+                    float acc = 0.0f;
+                    for (int i = 0; i <= j; ++i) acc = fmaf(sn[D + packed(i, j)], s_x[i], acc);
+                    s_v[j] = acc;
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    float m = 0.0f, w2 = 0.0f;
+                    for (int i = 0; i < D; ++i) m = fmaf(sn[i], s_x[i], m);
+                    for (int j = 0; j < D; ++j) w2 = fmaf(s_v[j], s_v[j], w2);
+                    s_scal[2] = m;
+                    s_scal[3] = w2;
+                }
+            }
+            __syncthreads();
+        } else if (tid == 0) {
+            p.bad[inst] += 1;
+        }
+    }
+
+    if (!decide) {
+        if (tid == 0) {
+            p.aprev[inst] = -1;
+            if (inst == 0) p.hdr->pending = 0;
+        }
+        return;
+    }
+
+    if (!x_ok) {
+        if (p.scores != nullptr) {
+            float *sc = p.scores + (size_t)inst * 2 * K;
+            for (int k = tid; k < K; k += nthr) {
+                sc[k] = -INFINITY;
+                sc[K + k] = -INFINITY;
+            }
+        }
+        if (tid == 0) {
+            p.bad[inst] += 1;
+            p.aprev[inst] = -1;
+            if (p.action != nullptr) p.action[inst] = -1;
+            if (inst == 0) {
+                p.hdr->t = p.t_next;
+                p.hdr->pending = 1;
+            }
+        }
+        return;
+    }
+
+    // ---- phase 2: score every active arm (Eq. 1) ----
+    const int k = tid;
+    const uint32_t *mask = p.mask + (size_t)inst * p.KW;
+    const bool active = k < K && ((mask[k >> 5] >> (k & 31)) & 1u);
+    float m = 0.0f, w2 = 0.0f;
+    if (active && k != a_upd) {
+        const float4 *src = p.arms + rec_base + k;
+        const size_t stride = (size_t)K;
+        score_record<D>([&](int c) { return src[(size_t)c * stride]; }, x, m, w2);
+    }
+    if (k == a_upd) {
+        m = s_scal[2];
+        w2 = s_scal[3];
+    }
+    float ucb = -INFINITY, lcb = -INFINITY;
+    if (active) {
+        const float w = sqrtf(fmaxf(w2, 0.0f));
+        ucb = fmaf(p.alpha, w, m);
+        lcb = fmaf(-p.alpha, w, m);
+    }
+    if (p.scores != nullptr && k < K) {
+        float *sc = p.scores + (size_t)inst * 2 * K;
+        sc[k] = ucb;
+        sc[K + k] = lcb;
+    }
+
+    // ---- phase 3: pruning and argmax ----
+    bool keep = active;
+    if (p.prune_now) {
+        float l = active ? lcb : -INFINITY;
+        for (int off = kWave / 2; off > 0; off >>= 1) l = fmaxf(l, __shfl_xor(l, off));
+        if (lane == 0) s_red_v[wave] = l;
+        __syncthreads();
+        float lstar = -INFINITY;
+        for (int w = 0; w < nwave; ++w) lstar = fmaxf(lstar, s_red_v[w]);
+        keep = active && !(ucb < lstar);
+        __syncthreads();
+    }
+    const unsigned long long bal = __ballot(keep);
+    if (p.prune_now) {
+        uint32_t *mw = p.mask + (size_t)inst * p.KW;
+        const int w0 = 2 * wave;
+        if (lane == 0 && w0 < p.KW) mw[w0] = (uint32_t)(bal & 0xffffffffull);
+        if (lane == 0 && w0 + 1 < p.KW) mw[w0 + 1] = (uint32_t)(bal >> 32);
+    }
+    BestPair b{keep ? ucb : -INFINITY, keep ? k : 0x7fffffff};
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        BestPair o{__shfl_xor(b.v, off), __shfl_xor(b.k, off)};
+        b = better(b, o);
+    }
+    if (lane == 0) {
+        s_red_v[wave] = b.v;
+        s_red_k[wave] = b.k;
+        s_red_n[wave] = __popcll(bal);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        BestPair best{s_red_v[0], s_red_k[0]};
+        int n = s_red_n[0];
+        for (int w = 1; w < nwave; ++w) {
+            best = better(best, BestPair{s_red_v[w], s_red_k[w]});
+            n += s_red_n[w];
+        }
+        const int a = best.k == 0x7fffffff ? -1 : best.k;
+        if (p.action != nullptr) p.action[inst] = a;
+        p.aprev[inst] = a;
+        p.kact[inst] = n;
+        if (inst == 0) {
+            p.hdr->t = p.t_next;
+            p.hdr->pending = 1;
+        }
+    }
+    if (tid < D) p.xprev[(size_t)inst * D + tid] = x[tid];
+}
+
+// ---- initialisation and export ----
+
+struct InitArgs {
+    float4 *arms;
+    uint32_t *mask;
+    float *xprev;
+    int32_t *aprev;
+    int32_t *kact;
+    int32_t *nsel;
+    int32_t *bad;
+    StateHeader *hdr;
+    StateHeader h;
+    int32_t B, K, KW, d, C;
+    float inv_sqrt_lambda;
+};
+
+__global__ void agft_init_kernel(InitArgs p) {
+    const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t gsz = (size_t)gridDim.x * blockDim.x;
+    const size_t nrec = (size_t)p.B * p.C * p.K;
+    const int nt = p.d / 4;
+    for (size_t idx = gtid; idx < nrec; idx += gsz) {
+        const int c = (int)((idx / p.K) % p.C);
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        if (c >= nt) {
+            for (int q = 0; q < 4; ++q) {
+                int i, j;
+                unpack(4 * (c - nt) + q, i, j);
+                v[q] = (i == j) ? p.inv_sqrt_lambda : 0.0f;
+            }
+        }
+        p.arms[idx] = make_float4(v[0], v[1], v[2], v[3]);
+    }
+    const size_t nmask = (size_t)p.B * p.KW;
+    for (size_t idx = gtid; idx < nmask; idx += gsz) {
+        const int w = (int)(idx % p.KW);
+        const int rem = p.K - 32 * w;
+        p.mask[idx] = rem >= 32 ? 0xffffffffu : ((1u << rem) - 1u);
+    }
+    for (size_t idx = gtid; idx < (size_t)p.B * p.d; idx += gsz) p.xprev[idx] = 0.0f;
+    for (size_t idx = gtid; idx < (size_t)p.B * p.K; idx += gsz) p.nsel[idx] = 0;
+    for (size_t idx = gtid; idx < (size_t)p.B; idx += gsz) {
+        p.aprev[idx] = -1;
+        p.kact[idx] = p.K;
+        p.bad[idx] = 0;
+    }
+    if (gtid == 0) *p.hdr = p.h;
+}
+
+template <int D>
+__global__ void agft_export_kernel(const float4 *arms, int B, int K, float *theta, float *ainv) {
+    using R = Rec<D>;
+    const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= (size_t)B * K) return;
+    const size_t inst = gid / K;
+    const int k = (int)(gid % K);
+    float rec[R::F];
+    for (int c = 0; c < R::C; ++c) {
+        const float4 v = arms[(inst * R::C + c) * K + k];
+        rec[4 * c + 0] = v.x;
+        rec[4 * c + 1] = v.y;
+        rec[4 * c + 2] = v.z;
+        rec[4 * c + 3] = v.w;
+    }
+    if (theta != nullptr)
+        for (int i = 0; i < D; ++i) theta[gid * D + i] = rec[i];
+    if (ainv != nullptr) {
+        const float *S = rec + D;
+        for (int r = 0; r < D; ++r)
+            for (int c = 0; c < D; ++c) {
+                float acc = 0.0f;
+                for (int j = (r > c ? r : c); j < D; ++j) acc = fmaf(S[packed(r, j)], S[packed(c, j)], acc);
+                ainv[(gid * D + r) * D + c] = acc;
+            }
+    }
+}
+
+}  // namespace
+
+// ---- C ABI ----
+
+struct agft_handle {
+    agft_config cfg;
+    Layout lay;
+    char *base;
+    hipStream_t stream;
+    int64_t t;
+    int pending;
+};
+
+namespace {
+
+bool config_ok(const agft_config *c) {
+    if (c == nullptr) return false;
+    if (c->B < 1 || c->K < 1 || c->K > kMaxK) return false;
+    if (!std::isfinite(c->lambda) || !(c->lambda > 0.0f)) return false;
+    if (!std::isfinite(c->alpha0) || c->alpha0 < 0.0f) return false;
+    if (c->alpha_sched != 0 && c->alpha_sched != 1) return false;
+    if (c->prune_rule != 0 && c->prune_rule != 1) return false;
+    if (c->prune_period < 1) return false;
+    if ((c->flags & ~AGFT_ADOPT_STATE) != 0) return false;
+    return true;
+}
+
+bool dim_supported(int d) { return d == 8 || d == 16 || d == 32; }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? AGFT_OK : AGFT_E_HIP; }
+
+StateHeader make_header(const agft_config *c) {
+    StateHeader h;
+    std::memset(&h, 0, sizeof(h));
+    h.magic = kMagic;
+    h.version = AGFT_ABI_VERSION;
+    h.B = c->B;
+    h.K = c->K;
+    h.d = c->d;
+    h.chunks = chunks_for(c->d);
+    h.mask_words = (c->K + 31) / 32;
+    h.pending = 0;
+    h.t = 0;
+    h.lambda = c->lambda;
+    h.alpha0 = c->alpha0;
+    h.alpha_sched = c->alpha_sched;
+    h.prune_rule = c->prune_rule;
+    h.prune_period = c->prune_period;
+    return h;
+}
+
+template <class T>
+T *at(char *base, size_t off) {
+    return reinterpret_cast<T *>(base + off);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t agft_state_bytes(const agft_config *cfg) {
+    if (!config_ok(cfg) || !dim_supported(cfg->d)) return 0;
+    return layout_for(cfg->B, cfg->K, cfg->d).total;
+}
+
+int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stream, agft_handle **out) {
+    if (out == nullptr) return AGFT_E_INVAL;
+    *out = nullptr;
+    if (!config_ok(cfg) || d_state == nullptr) return AGFT_E_INVAL;
+    if (!dim_supported(cfg->d)) return AGFT_E_UNSUPPORTED;
+    if (reinterpret_cast<uintptr_t>(d_state) % kAlign != 0) return AGFT_E_INVAL;
+    const Layout lay = layout_for(cfg->B, cfg->K, cfg->d);
+    if (nbytes < lay.total) return AGFT_E_INVAL;
+    agft_handle *h = new (std::nothrow) agft_handle;
+    if (h == nullptr) return AGFT_E_INVAL;
+    h->cfg = *cfg;
+    h->lay = lay;
+    h->base = static_cast<char *>(d_state);
+    h->stream = static_cast<hipStream_t>(stream);
+    h->t = 0;
+    h->pending = 0;
+    const StateHeader want = make_header(cfg);
+    if (cfg->flags & AGFT_ADOPT_STATE) {
+        StateHeader got;
+        hipError_t e = hipMemcpyAsync(&got, d_state, sizeof(got), hipMemcpyDeviceToHost, h->stream);
+        if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
+        if (e != hipSuccess) {
+            delete h;
+            return AGFT_E_HIP;
+        }
+        if (got.magic != kMagic || got.version != want.version || got.B != want.B || got.K != want.K ||
+            got.d != want.d || got.chunks != want.chunks || got.t < 0 ||
+            (got.pending != 0 && got.pending != 1)) {
+            delete h;
+            return AGFT_E_STATE;
+        }
+        h->t = got.t;
+        h->pending = got.pending;
+        *out = h;
+        return AGFT_OK;
+    }
+    InitArgs a;
+    a.arms = at<float4>(h->base, lay.arms);
+    a.mask = at<uint32_t>(h->base, lay.mask);
+    a.xprev = at<float>(h->base, lay.xprev);
+    a.aprev = at<int32_t>(h->base, lay.aprev);
+    a.kact = at<int32_t>(h->base, lay.kact);
+    a.nsel = at<int32_t>(h->base, lay.nsel);
+    a.bad = at<int32_t>(h->base, lay.bad);
+    a.hdr = at<StateHeader>(h->base, 0);
+    a.h = want;
+    a.B = cfg->B;
+    a.K = cfg->K;
+    a.KW = (cfg->K + 31) / 32;
+    a.d = cfg->d;
+    a.C = chunks_for(cfg->d);
+    a.inv_sqrt_lambda = (float)(1.0 / std::sqrt((double)cfg->lambda));
+    const size_t work = (size_t)cfg->B * a.C * cfg->K;
+    size_t blocks = (work + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(agft_init_kernel, dim3((unsigned)blocks), dim3(256), 0, h->stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        delete h;
+        return AGFT_E_HIP;
+    }
+    *out = h;
+    return AGFT_OK;
+}
+
+int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t *d_action, float *d_scores) {
+    if (h == nullptr) return AGFT_E_INVAL;
+    if (h->pending && d_reward == nullptr) return AGFT_E_STATE;
+    const agft_config &c = h->cfg;
+    StepArgs p;
+    p.arms = at<float4>(h->base, h->lay.arms);
+    p.mask = at<uint32_t>(h->base, h->lay.mask);
+    p.xprev = at<float>(h->base, h->lay.xprev);
+    p.aprev = at<int32_t>(h->base, h->lay.aprev);
+    p.kact = at<int32_t>(h->base, h->lay.kact);
+    p.nsel = at<int32_t>(h->base, h->lay.nsel);
+    p.bad = at<int32_t>(h->base, h->lay.bad);
+    p.hdr = at<StateHeader>(h->base, 0);
+    p.ctx = d_ctx;
+    p.reward = d_reward;
+    p.action = d_ctx != nullptr ? d_action : nullptr;
+    p.scores = d_ctx != nullptr ? d_scores : nullptr;
+    p.B = c.B;
+    p.K = c.K;
+    p.KW = (c.K + 31) / 32;
+    p.apply_update = h->pending;
+    const int64_t t = h->t;
+    p.prune_now = (d_ctx != nullptr && c.prune_rule == 1 && t > 0 && t % c.prune_period == 0) ? 1 : 0;
+    p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
+    p.t_next = d_ctx != nullptr ? t + 1 : t;
+    const int threads = ((c.K + kWave - 1) / kWave) * kWave;
+    const dim3 grid((unsigned)c.B), block((unsigned)threads);
+    switch (c.d) {
+        case 8: hipLaunchKernelGGL(agft_step_kernel<8>, grid, block, 0, h->stream, p); break;
+        case 16: hipLaunchKernelGGL(agft_step_kernel<16>, grid, block, 0, h->stream, p); break;
+        case 32: hipLaunchKernelGGL(agft_step_kernel<32>, grid, block, 0, h->stream, p); break;
+        default: return AGFT_E_UNSUPPORTED;
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return AGFT_E_HIP;
+    if (d_ctx != nullptr) {
+        h->t = t + 1;
+        h->pending = 1;
+    } else {
+        h->pending = 0;
+    }
+    return AGFT_OK;
+}
+
+int agft_get_state(const agft_handle *h, agft_state_view *out) {
+    if (h == nullptr || out == nullptr) return AGFT_E_INVAL;
+    out->t = h->t;
+    out->pending = h->pending;
+    out->B = h->cfg.B;
+    out->K = h->cfg.K;
+    out->d = h->cfg.d;
+    out->chunks = chunks_for(h->cfg.d);
+    out->mask_words = (h->cfg.K + 31) / 32;
+    out->arms = h->base + h->lay.arms;
+    out->mask = at<uint32_t>(h->base, h->lay.mask);
+    out->xprev = at<float>(h->base, h->lay.xprev);
+    out->aprev = at<int32_t>(h->base, h->lay.aprev);
+    out->kact = at<int32_t>(h->base, h->lay.kact);
+    out->nsel = at<int32_t>(h->base, h->lay.nsel);
+    out->bad = at<int32_t>(h->base, h->lay.bad);
+    return AGFT_OK;
+}
+
+int agft_export(agft_handle *h, float *d_theta, float *d_ainv) {
+    if (h == nullptr) return AGFT_E_INVAL;
+    if (d_theta == nullptr && d_ainv == nullptr) return AGFT_OK;
+    const agft_config &c = h->cfg;
+    const size_t n = (size_t)c.B * c.K;
+    const dim3 grid((unsigned)((n + 127) / 128)), block(128);
+    const float4 *arms = at<float4>(h->base, h->lay.arms);
+    switch (c.d) {
+        case 8: hipLaunchKernelGGL(agft_export_kernel<8>, grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv); break;
+        case 16: hipLaunchKernelGGL(agft_export_kernel<16>, grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv); break;
+        case 32: hipLaunchKernelGGL(agft_export_kernel<32>, grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv); break;
+        default: return AGFT_E_UNSUPPORTED;
+    }
+    return hip_status(hipGetLastError());
+}
+
+int agft_set_stream(agft_handle *h, void *stream) {
+    if (h == nullptr) return AGFT_E_INVAL;
+    h->stream = static_cast<hipStream_t>(stream);
+    return AGFT_OK;
+}
+
+int agft_destroy(agft_handle *h) {
+    delete h;
+    return AGFT_OK;
+}
+
+const char *agft_strerror(int code) {
+    switch (code) {
+        case AGFT_OK: return "ok";
+        case AGFT_E_INVAL: return "invalid argument";
+        case AGFT_E_UNSUPPORTED: return "unsupported configuration";
+        case AGFT_E_STATE: return "call not valid in the current state";
+        case AGFT_E_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int agft_abi_version(void) { return AGFT_ABI_VERSION; }
+
+}  // extern "C"

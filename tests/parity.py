@@ -1,0 +1,145 @@
+"""Comparison of recorded GPU runs with the fp64 oracle.
+
+The oracle makes its own decisions.  Only where the paper's method admits
+several answers does it take the GPU's: an arm whose UCB is within TIE of the
+best (the argmax is not unique at the precision the scores carry) and a prune
+decision whose UCB is within TIE of the threshold.  Exact ties in the oracle
+(arms with bit-identical scores, e.g. untouched arms) are not ambiguous: the
+lowest index must win on both sides.
+
+Closed loop (compare): the oracle also runs its own fp64 environment on the
+same exogenous draws, so GPU contexts and rewards are checked too.
+Open loop (compare_open_loop): both sides get the same given contexts and
+rewards.
+"""
+import numpy as np
+
+from agft_workloads import exogenous
+from oracle import Oracle, run_closed_loop
+
+SCORE_TOL = 1e-4   # |s_gpu - s_oracle| <= SCORE_TOL * max(1, |s_oracle|)
+TIE = 1e-5         # score gaps at or below this (times max(1, |score|)) are near-ties
+ENV_TOL = 1e-5     # contexts and rewards: fp32 environment vs fp64 environment
+
+
+def mask_words_to_bool(words, K):
+    words = np.asarray(words).astype(np.int64) & 0xFFFFFFFF
+    k = np.arange(K)
+    return ((words[..., k // 32] >> (k % 32)) & 1).astype(bool)
+
+
+class ParityError(AssertionError):
+    pass
+
+
+class Checker:
+    def __init__(self, name, K, ids, g_a, g_keep, g_s=None, g_x=None, g_r=None):
+        self.name, self.K, self.ids = name, K, list(ids)
+        self.g_a, self.g_keep, self.g_s, self.g_x, self.g_r = g_a, g_keep, g_s, g_x, g_r
+        self.st = dict(max_score_err=0.0, max_ctx_err=0.0, max_reward_err=0.0, forced=0,
+                       forced_prune=0, exact_tie_steps=0, decisions=0, no_decision=0)
+
+    def fail(self, msg):
+        raise ParityError(f"{self.name}: {msg}")
+
+    def __call__(self, t, x, r_prev, ucb, lcb, keep, action):
+        st, ids = self.st, self.ids
+        if self.g_x is not None:
+            ex = np.abs(self.g_x[t] - x) / np.maximum(1.0, np.abs(x))
+            ex = np.where(np.isfinite(x), ex, 0.0)
+            st["max_ctx_err"] = max(st["max_ctx_err"], float(ex.max()))
+            if ex.max() > ENV_TOL:
+                i = int(np.argmax(ex.max(axis=1)))
+                self.fail(f"context mismatch at t={t}, instance {ids[i]}: {self.g_x[t, i]} vs {x[i]}")
+        if self.g_r is not None and t > 0:
+            er = np.abs(self.g_r[t - 1] - r_prev) / np.maximum(1.0, np.abs(r_prev))
+            st["max_reward_err"] = max(st["max_reward_err"], float(er.max()))
+            if er.max() > ENV_TOL:
+                self.fail(f"reward mismatch at t={t - 1}: max rel err {er.max():.3e}")
+        act = np.isfinite(ucb)
+        if self.g_s is not None:
+            if not np.array_equal(np.isfinite(self.g_s[t, :, 0]), act):
+                self.fail(f"active sets differ at t={t}")
+            for row, ref in ((0, ucb), (1, lcb)):
+                err = np.where(act, np.abs(self.g_s[t, :, row] - ref) / np.maximum(1.0, np.abs(ref)), 0.0)
+                st["max_score_err"] = max(st["max_score_err"], float(err.max()))
+                if err.max() > SCORE_TOL:
+                    i, k = np.unravel_index(int(np.argmax(err)), err.shape)
+                    self.fail(f"score mismatch at t={t}, instance {ids[i]}, arm {k}: "
+                              f"{self.g_s[t, i, row, k]!r} vs {ref[i, k]!r}")
+        commit_keep = keep.copy()
+        commit_a = action.copy()
+        for i in range(len(ids)):
+            ga = int(self.g_a[t, i])
+            if action[i] < 0:
+                st["no_decision"] += 1
+                if ga != -1:
+                    self.fail(f"GPU decided on a non-finite context at t={t}, instance {ids[i]}")
+                continue
+            if not np.array_equal(self.g_keep[t, i], keep[i]):
+                lstar = lcb[i][act[i]].max()
+                diff = np.flatnonzero(self.g_keep[t, i] != keep[i])
+                amb = np.abs(ucb[i, diff] - lstar) <= TIE * max(1.0, abs(lstar))
+                if not amb.all():
+                    self.fail(f"prune mismatch at t={t}, instance {ids[i]}, arms {diff[~amb]}")
+                st["forced_prune"] += 1
+                commit_keep[i] = self.g_keep[t, i]
+            kp = commit_keep[i]
+            u = np.where(kp, ucb[i], -np.inf)
+            ustar = u.max()
+            own = int(np.flatnonzero(u == ustar)[0])
+            near = np.flatnonzero(kp & (ustar - ucb[i] <= TIE * max(1.0, abs(ustar))))
+            st["decisions"] += 1
+            if ga not in near:
+                gu = ucb[i, ga] if 0 <= ga < self.K else None
+                self.fail(f"action mismatch at t={t}, instance {ids[i]}: GPU {ga} (UCB {gu}), "
+                          f"oracle {own} (UCB {ustar})")
+            if len(near) > 1 and np.all(ucb[i, near] == ustar):
+                st["exact_tie_steps"] += 1
+                if ga != own:
+                    self.fail(f"exact tie broken wrongly at t={t}, instance {ids[i]}: {ga} vs {own}")
+            if ga != own:
+                st["forced"] += 1
+            commit_a[i] = ga
+        return commit_a, commit_keep
+
+    def finish(self):
+        self.st["forced_rate"] = self.st["forced"] / max(1, self.st["decisions"])
+        return self.st
+
+
+def compare(wl, T, probes, rec):
+    """Closed loop: replay the probe instances through the oracle and its
+    environment; raise ParityError on a violation.  rec: host tensors from
+    paper_2508_01744_amd.run_closed_loop(probes=...)."""
+    probes = list(probes)
+    arrivals, noise = exogenous(wl, probes, T)
+    chk = Checker(wl.name, wl.K, probes, rec["a"].numpy(),
+                  mask_words_to_bool(rec["mask"].numpy(), wl.K),
+                  rec["scores"].numpy().astype(np.float64) if "scores" in rec else None,
+                  rec["x"].numpy().astype(np.float64), rec["r"].numpy().astype(np.float64))
+    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk)
+    st = chk.finish()
+    st["oracle"] = out["oracle"]
+    return st
+
+
+def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s):
+    """Open loop: contexts X [T][B][d] and rewards R [T][B] (reward of the
+    decision at t) given to both sides.  cfg: dict(B, K, d, lam, alpha0,
+    sched, prune, period).  GPU records: actions [T][B], mask words
+    [T][B][KW] after each step, scores [T][B][2][K]."""
+    T = X.shape[0]
+    ora = Oracle(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
+                 cfg["prune"], cfg["period"])
+    chk = Checker(name, cfg["K"], range(cfg["B"]), g_a, mask_words_to_bool(g_masks, cfg["K"]), g_s)
+    r_prev = None
+    for t in range(T):
+        ucb, lcb, keep, action = ora.decide(X[t], r_prev)
+        a, k = chk(t, X[t], r_prev, ucb, lcb, keep, action)
+        ora.commit(X[t], a, k)
+        r_prev = R[t]
+    ora.flush(r_prev)
+    st = chk.finish()
+    st["oracle"] = ora
+    return st

@@ -1,0 +1,110 @@
+"""The C ABI library loads, exports every declared symbol and rejects bad
+arguments before touching the GPU (CPU only: no call here launches work)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2508_01744_amd._lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = []
+    for hdr in ("agft.h", "agft_sim.h"):
+        text = open(os.path.join(ROOT, "include", hdr)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names += re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\**\s*(agft_[a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return L.lib()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(L.EXPORTED)
+
+
+def test_abi_version_and_strerror(lib):
+    assert L.agft_abi_version() == 1
+    for code in (0, -1, -2, -3, -4):
+        assert L.agft_strerror(code)
+    assert L.agft_strerror(-99) == "unknown status"
+
+
+def _cfg(**kw):
+    base = dict(B=4, K=16, d=8, lambda_=1.0, alpha0=0.5, alpha_sched=0, prune_rule=0,
+                prune_period=50, flags=0)
+    base.update(kw)
+    return L.agft_config(**base)
+
+
+def test_state_bytes(lib):
+    n = L.agft_state_bytes(_cfg())
+    assert n > 0 and n % 256 == 0
+    # arms region: B * (d/4 + d(d+1)/8) chunks * K * 16 bytes dominates
+    big = L.agft_state_bytes(_cfg(B=65536, K=128, d=16))
+    assert big >= 65536 * 38 * 128 * 16
+    assert big < 65536 * 38 * 128 * 16 * 1.02
+    for bad in (dict(B=0), dict(K=0), dict(K=1025), dict(lambda_=0.0), dict(lambda_=float("nan")),
+                dict(alpha0=-1.0), dict(alpha0=float("inf")), dict(alpha_sched=2),
+                dict(prune_rule=3), dict(prune_period=0), dict(flags=4), dict(d=12)):
+        assert L.agft_state_bytes(_cfg(**bad)) == 0, bad
+
+
+def test_create_rejects_before_launch(lib):
+    cfg = _cfg()
+    n = L.agft_state_bytes(cfg)
+    code, h = L.agft_create(cfg, None, n, None)
+    assert code == L.AGFT_E_INVAL and not h.value
+    code, h = L.agft_create(cfg, ctypes.c_void_p(0x1001), n, None)   # misaligned
+    assert code == L.AGFT_E_INVAL
+    code, h = L.agft_create(cfg, ctypes.c_void_p(0x100000), n - 1, None)  # too small
+    assert code == L.AGFT_E_INVAL
+    code, h = L.agft_create(_cfg(d=12), ctypes.c_void_p(0x100000), 1 << 30, None)
+    assert code == L.AGFT_E_UNSUPPORTED
+    code, h = L.agft_create(_cfg(alpha0=-1.0), ctypes.c_void_p(0x100000), 1 << 30, None)
+    assert code == L.AGFT_E_INVAL
+    assert lib.agft_create(ctypes.byref(cfg), ctypes.c_void_p(0x100000), n, None, None) == L.AGFT_E_INVAL
+
+
+def test_null_handle_calls(lib):
+    assert L.agft_step(None, None, None, None, None) == L.AGFT_E_INVAL
+    code, _ = L.agft_get_state(None)
+    assert code == L.AGFT_E_INVAL
+    assert L.agft_export(None, None, None) == L.AGFT_E_INVAL
+    assert L.agft_set_stream(None, None) == L.AGFT_E_INVAL
+    assert L.agft_destroy(None) == L.AGFT_OK
+
+
+def _env_cfg(**kw):
+    from agft_workloads import ENV, get_workload
+    from paper_2508_01744_amd.env import env_config
+    cfg = env_config(get_workload(2, B=8, T=10), ENV)
+    for k, v in kw.items():
+        setattr(cfg, k, v)
+    return cfg
+
+
+def test_env_validation(lib):
+    assert L.agft_env_state_bytes(_env_cfg()) > 0
+    for bad in (dict(B=0), dict(K=0), dict(d=7), dict(T=0), dict(lat_min=0.0), dict(f_lo=0.0),
+                dict(tpot_div=0.0), dict(svc_lo=0), dict(q_cap=-1)):
+        assert L.agft_env_state_bytes(_env_cfg(**bad)) == 0, bad
+    cfg = _env_cfg()
+    n = L.agft_env_state_bytes(cfg)
+    p = ctypes.c_void_p(0x100000)
+    assert L.agft_env_reset(cfg, None, n, p, p, p, None) == L.AGFT_E_INVAL
+    assert L.agft_env_reset(cfg, ctypes.c_void_p(0x1001), n, p, p, p, None) == L.AGFT_E_INVAL
+    assert L.agft_env_reset(cfg, p, n - 1, p, p, p, None) == L.AGFT_E_INVAL
+    assert L.agft_env_step(cfg, p, n, -1, p, p, p, p, p, None) == L.AGFT_E_INVAL
+    assert L.agft_env_step(cfg, p, n, cfg.T, p, p, p, p, p, None) == L.AGFT_E_INVAL
+    assert L.agft_env_step(cfg, p, n, 0, None, p, p, p, p, None) == L.AGFT_E_INVAL
