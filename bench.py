@@ -1,0 +1,221 @@
+"""Benchmark of the batched AGFT decide-and-update step on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload cfg4]
+
+A step is one decision for every instance of the workload: the tuner step
+kernel (pending update, scoring of every active arm, pruning, argmax) and the
+environment kernel that produces the next contexts and rewards.  All inputs
+(state, exogenous draws) are resident in HBM before the timed region, which
+times exactly K steps from a freshly initialised state.  Prints one JSON line.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, AMD's published peak
+STEP_SRC = os.path.join(ROOT, "paper_2508_01744_amd", "csrc", "agft_step.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "agft_step_counters.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash(path=STEP_SRC):
+    with open(path, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()[:16]
+
+
+def record_floats(d):
+    return d + d * (d + 1) // 2
+
+
+def step_bytes(wl, kact_total, prune_step, update):
+    """Algorithmic HBM bytes of one step kernel launch.
+
+    Per instance: the active arms' records are read once (the previous
+    decision's arm in the update phase, the others in the scoring phase), the
+    updated record is written once; plus context, stashed context, reward,
+    action, bookkeeping words and the action-set mask (written at pruning
+    steps).  kact_before: active arms per instance when the step starts.
+    """
+    s = record_floats(wl.d)
+    kw = (wl.K + 31) // 32
+    records = 4 * s * (kact_total + (wl.B if update else 0))
+    io = wl.B * 4 * (3 * wl.d + 7)     # ctx, xprev r/w; reward, action, aprev r/w, kact, nsel r/w
+    mask = wl.B * 4 * kw * (2 if prune_step else 1)
+    return float(records + io + mask)
+
+
+def cpu_baseline(wl, budget_s):
+    """The fp64 oracle (C, OpenMP over instances) with its fp64 environment,
+    closed loop, on a bounded sample of the workload's instances and steps."""
+    import numpy as np
+    from agft_workloads import exogenous
+    from oracle import Env, Oracle
+    n = min(wl.B, 4096)
+    T = wl.T
+    arr, noi = exogenous(wl, range(n), T)
+    env = Env(wl, arr, noi, T)
+    ora = Oracle.from_workload(wl, B=n)
+    x = env.reset()
+    r = None
+    t0 = time.perf_counter()
+    steps = 0
+    for t in range(T):
+        ucb, lcb, keep, action = ora.decide(x, r)
+        ora.commit(x, action, keep)
+        r, x = env.step(t, action)
+        steps += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    el = time.perf_counter() - t0
+    return dict(value=n * steps / el, unit="decision-steps/s", cores=Oracle.threads(), kind="oracle",
+                sample=f"{n} instances x {steps} steps of {wl.name} (closed loop with the fp64 "
+                       f"environment, {el:.1f} s)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's T)")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="cfg4")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds for the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run a plain 1 GiB copy kernel (for counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the tuner instances are independent, so a "
+              f"multi-GPU run is the same kernel on B/N instances per GPU (got --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from agft_workloads import ENV, exogenous, get_workload
+    from paper_2508_01744_amd import GpuEnv, Tuner, env_config
+
+    wl = get_workload(args.workload)
+    K = wl.T if args.steps is None else args.steps
+    W = args.warmup
+    T_env = max(K, W, 1)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log(f"[bench] {wl.name}: B={wl.B} K={wl.K} d={wl.d}; timed steps {K}, warmup {W}")
+
+    arr, noi = exogenous(wl, T=T_env)
+    arr_d = torch.as_tensor(arr, device=dev)
+    noi_d = torch.as_tensor(noi, device=dev)
+    env = GpuEnv(env_config(wl, ENV, T=T_env), arr_d, noi_d)
+    tuner = Tuner.from_workload(wl, device=dev)
+    action = torch.empty(wl.B, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fresh():
+        nonlocal tuner
+        state = tuner.state
+        tuner.close()
+        tuner = Tuner.from_workload(wl, device=dev, state=state)
+
+    def run(nsteps, kernel_events=None, kact_log=None):
+        x = env.reset()
+        r = None
+        for t in range(nsteps):
+            if kact_log is not None:
+                kact_log.append(tuner.view()["kact"].sum())
+            if kernel_events is not None:
+                kernel_events[t][0].record(stream)
+            tuner.step(x, r, action)
+            if kernel_events is not None:
+                kernel_events[t][1].record(stream)
+            r, x = env.step(t, action)
+
+    # warm-up on a fresh state, then re-initialise
+    if W > 0:
+        run(W)
+    torch.cuda.synchronize()
+    fresh()
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    run(K, kernel_events=ev)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    elapsed_ms = start.elapsed_time(stop)
+    kernel_ms = np.array([a.elapsed_time(b) for a, b in ev])
+
+    # the run is deterministic: replay it untimed to log the active-arm counts
+    fresh()
+    kact_log = []
+    run(K, kact_log=kact_log)
+    kact_before = [int(v) for v in torch.stack(kact_log).cpu()] if kact_log else []
+    torch.cuda.synchronize()
+
+    if args.calibrate_copy:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev).normal_()
+        b = torch.empty_like(a)
+        for _ in range(3):
+            torch.neg(a, out=b)
+        torch.cuda.synchronize()
+        del a, b
+
+    total_bytes = 0.0
+    for t in range(K):
+        prune_step = wl.prune == 1 and t > 0 and t % wl.period == 0
+        total_bytes += step_bytes(wl, kact_before[t], prune_step, update=t > 0)
+    bytes_per_launch = total_bytes / K
+    kernel_avg_ms = float(kernel_ms.mean())
+    achieved = bytes_per_launch / (kernel_avg_ms * 1e-3) / 1e9
+
+    traffic = None
+    if os.path.exists(COUNTERS):
+        with open(COUNTERS) as fh:
+            cnt = json.load(fh)
+        if cnt.get("source_sha256_16") == source_hash() and cnt.get("workload") == wl.name:
+            traffic = cnt.get("hbm_bytes_per_launch")
+
+    value = wl.B * K / (elapsed_ms * 1e-3)
+    res = {
+        "metric": "bandit decision-steps/sec (instances x steps) + achieved HBM GB/s vs peak",
+        "value": value,
+        "unit": "decision-steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": elapsed_ms / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded load traces, closed-form energy-delay reward)",
+        "config": {"workload": f"{wl.name}: {wl.description}", "instances": wl.B, "arms": wl.K,
+                   "context_dim": wl.d, "steps_per_run": wl.T, "parallelism": "none (1 GPU)"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
+        "detail": {"step_kernel_avg_ms": kernel_avg_ms,
+                   "step_kernel_share": float(kernel_ms.sum() / elapsed_ms),
+                   "algorithmic_bytes_per_launch": bytes_per_launch,
+                   "mean_active_arms": float(np.mean(kact_before) / wl.B) if kact_before else None,
+                   "wall_s": t_wall},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the fp64 oracle on the host")
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -9,14 +9,15 @@
 // memory.
 //
 // Per step and instance (Sec. 4.2):
-//   phase 1  fold the previous decision's reward into its arm: Eq. 3-5 as a
-//            square-root rank-1 update of S (below) plus the matching theta
-//            update, staged in LDS, written back, and the updated arm scored
-//            on x_t from LDS;
-//   phase 2  every other active arm: v = S^T x_t, w^2 = |v|^2, m = theta^T x_t,
-//            UCB = m + alpha_t w, LCB = m - alpha_t w  (Eq. 1);
-//   phase 3  pruning when due (drop UCB_k < max_j LCB_j), argmax with ties to
-//            the lowest arm index, epilogue.
+//   1. fetch the record of the previous decision's arm (its update waits);
+//   2. every other active arm: v = S^T x_t, w^2 = |v|^2, m = theta^T x_t,
+//      UCB = m + alpha_t w, LCB = m - alpha_t w  (Eq. 1);
+//   3. fold the previous decision's reward into its arm: Eq. 3-5 as a
+//      square-root rank-1 update of S (below) plus the matching theta
+//      update, staged in LDS and written back; the updated arm is scored on
+//      x_t from LDS in the same operation order as the stream;
+//   4. pruning when due (drop UCB_k < max_j LCB_j), argmax with ties to the
+//      lowest arm index, epilogue.
 //
 // Square-root update.  Eq. 3 adds x x^T to A, so P = A^{-1} changes by the
 // Sherman-Morrison identity P' = P - P x x^T P / (1 + x^T P x).  With P = S S^T
@@ -162,6 +163,14 @@ struct StepArgs {
     int64_t t_next;        // t after this call (header bookkeeping)
 };
 
+// Streaming load that bypasses cache retention: every record is read once
+// per step and the state of a large batch is many times the cache size.
+typedef float nt_f4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ld_nt(const float4 *p) {
+    const nt_f4 v = __builtin_nontemporal_load(reinterpret_cast<const nt_f4 *>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
 struct BestPair {
     float v;
     int k;
@@ -175,6 +184,8 @@ __device__ inline BestPair better(BestPair a, BestPair b) {
 template <int D>
 __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
     using R = Rec<D>;
+    // chunks of the updated record each thread loads (workgroups have >= 64 threads)
+    constexpr int NQ = (R::C + kWave - 1) / kWave;
     const int inst = blockIdx.x;
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;
@@ -201,7 +212,7 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
 
     // Context of this decision: uniform across the workgroup.
     float x[D];
-    bool x_ok = true;
+    bool x_ok = decide;
     if (decide) {
         const float *xi = p.ctx + (size_t)inst * D;
 #pragma unroll
@@ -214,81 +225,124 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
         for (int q = 0; q < D; ++q) x[q] = 0.0f;
     }
 
-    // ---- phase 1: pending update of the previous decision's arm ----
+    // Pending update of the previous decision's arm.  Its record and the
+    // stashed context are fetched first and consumed after the other arms
+    // have streamed, so their latency overlaps the stream.
     const int a_prev = p.apply_update ? p.aprev[inst] : -1;
-    int a_upd = -1;
-    if (a_prev >= 0 && a_prev < K) {
-        const float r = p.reward[inst];
-        if (isfinite(r)) {
-            a_upd = a_prev;
-            for (int c = tid; c < R::C; c += nthr) s_old[c] = p.arms[rec_base + (size_t)c * K + a_upd];
-            if (tid < D) s_xp[tid] = p.xprev[(size_t)inst * D + tid];
-            if (tid < D) s_x[tid] = x[tid];
-            __syncthreads();
-            const float *so = reinterpret_cast<const float *>(s_old);
-            const float *sth = so;             // theta
-            const float *sS = so + D;          // packed factor
+    const bool has_prev = a_prev >= 0 && a_prev < K;
+    const float r = has_prev ? p.reward[inst] : 0.0f;
+    const bool upd = has_prev && isfinite(r);
+    const int a_upd = upd ? a_prev : -1;
+    float4 old_chunk[NQ];
+    float xp_val = 0.0f;
+    if (upd) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int c = tid + q * nthr;
+            if (c < R::C) old_chunk[q] = p.arms[rec_base + (size_t)c * K + a_upd];
+        }
+        if (tid < D) xp_val = p.xprev[(size_t)inst * D + tid];
+    }
+
+    // ---- scoring of every other active arm (Eq. 1) ----
+    const int k = tid;
+    const uint32_t *mask = p.mask + (size_t)inst * p.KW;
+    const bool active = x_ok && k < K && ((mask[k >> 5] >> (k & 31)) & 1u);
+    float m = 0.0f, w2 = 0.0f;
+    if (active && k != a_upd) {
+        const float4 *src = p.arms + rec_base + k;
+        const size_t stride = (size_t)K;
+        score_record<D>([&](int c) { return ld_nt(&src[(size_t)c * stride]); }, x, m, w2);
+    }
+
+    // ---- square-root rank-1 update of the previous decision's arm ----
+    if (upd) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int c = tid + q * nthr;
+            if (c < R::C) s_old[c] = old_chunk[q];
+        }
+        if (tid < D) {
+            s_xp[tid] = xp_val;
+            s_x[tid] = x[tid];
+        }
+        __syncthreads();
+        const float *so = reinterpret_cast<const float *>(s_old);
+        const float *sth = so;             // theta
+        const float *sS = so + D;          // packed factor
+        if (tid < D) {
+            // f_j = sum_{i<=j} S_ij xp_i
+            const int j = tid;
+            float acc = 0.0f;
+            for (int i = 0; i <= j; ++i) acc = fmaf(sS[packed(i, j)], s_xp[i], acc);
+            s_f[j] = acc;
+        }
+        __syncthreads();
+        if (tid < kWave) {
+            // alpha_j = 1 + f_0^2 + ... + f_j^2 by a wavefront scan, the
+            // column coefficients, and the prediction error r - xp^T theta
+            const float fj = tid < D ? s_f[tid] : 0.0f;
+            float incl = fj * fj;
+#pragma unroll
+            for (int off = 1; off < D; off <<= 1) {
+                const float y = __shfl_up(incl, off);
+                if (lane >= off) incl += y;
+            }
+            float pred = tid < D ? s_xp[tid] * sth[tid] : 0.0f;
+#pragma unroll
+            for (int off = kWave / 2; off > 0; off >>= 1) pred += __shfl_xor(pred, off);
             if (tid < D) {
-                // f_j = sum_{i<=j} S_ij xp_i
+                const float al = 1.0f + incl;
+                const float al_prev = 1.0f + (incl - fj * fj);
+                s_ca[tid] = sqrtf(al_prev / al);
+                s_cb[tid] = fj / sqrtf(al_prev * al);
+                if (tid == D - 1) s_scal[0] = al;
+            }
+            if (tid == 0) s_scal[1] = r - pred;
+        }
+        __syncthreads();
+        float *sn = reinterpret_cast<float *>(s_new);
+        for (int e = tid; e < R::NSE; e += nthr) {
+            int i, j;
+            unpack(e, i, j);
+            float g = 0.0f;
+            for (int q = i; q < j; ++q) g = fmaf(s_f[q], sS[packed(i, q)], g);
+            sn[D + e] = s_ca[j] * sS[e] - s_cb[j] * g;
+        }
+        if (tid < D) {
+            // gain g_i = (S f)_i / alpha_{d-1}
+            const int i = tid;
+            float sf = 0.0f;
+            for (int q = i; q < D; ++q) sf = fmaf(sS[packed(i, q)], s_f[q], sf);
+            sn[i] = fmaf(sf / s_scal[0], s_scal[1], sth[i]);
+        }
+        __syncthreads();
+        for (int c = tid; c < R::C; c += nthr) p.arms[rec_base + (size_t)c * K + a_upd] = s_new[c];
+        if (tid == 0) p.nsel[(size_t)inst * K + a_upd] += 1;
+        if (x_ok) {
+            // score the updated arm on x_t from LDS, in the streaming order
+            if (tid < D) {
                 const int j = tid;
                 float acc = 0.0f;
-                for (int i = 0; i <= j; ++i) acc = fmaf(sS[packed(i, j)], s_xp[i], acc);
-                s_f[j] = acc;
+                for (int i = 0; i <= j; ++i) acc = fmaf(sn[D + packed(i, j)], s_x[i], acc);
+                s_v[j] = acc;
             }
             __syncthreads();
             if (tid == 0) {
-                float al = 1.0f;
-                for (int j = 0; j < D; ++j) {
-                    const float an = fmaf(s_f[j], s_f[j], al);
-                    s_ca[j] = sqrtf(al / an);
-                    s_cb[j] = s_f[j] / sqrtf(al * an);
-                    al = an;
-                }
-                float pred = 0.0f;
-                for (int i = 0; i < D; ++i) pred = fmaf(s_xp[i], sth[i], pred);
-                s_scal[0] = al;
-                s_scal[1] = r - pred;
+                float ma = 0.0f, w2a = 0.0f;
+                for (int i = 0; i < D; ++i) ma = fmaf(sn[i], s_x[i], ma);
+                for (int j = 0; j < D; ++j) w2a = fmaf(s_v[j], s_v[j], w2a);
+                s_scal[2] = ma;
+                s_scal[3] = w2a;
             }
             __syncthreads();
-            float *sn = reinterpret_cast<float *>(s_new);
-            for (int e = tid; e < R::NSE; e += nthr) {
-                int i, j;
-                unpack(e, i, j);
-                float g = 0.0f;
-                for (int k = i; k < j; ++k) g = fmaf(s_f[k], sS[packed(i, k)], g);
-                sn[D + e] = s_ca[j] * sS[e] - s_cb[j] * g;
+            if (k == a_upd) {
+                m = s_scal[2];
+                w2 = s_scal[3];
             }
-            if (tid < D) {
-                // gain g_i = (S f)_i / alpha_{d-1}
-                const int i = tid;
-                float sf = 0.0f;
-                for (int k = i; k < D; ++k) sf = fmaf(sS[packed(i, k)], s_f[k], sf);
-                sn[i] = fmaf(sf / s_scal[0], s_scal[1], sth[i]);
-            }
-            __syncthreads();
-            for (int c = tid; c < R::C; c += nthr) p.arms[rec_base + (size_t)c * K + a_upd] = s_new[c];
-            if (tid == 0) p.nsel[(size_t)inst * K + a_upd] += 1;
-            // score the updated arm on x_t from LDS, in the streaming path's order
-            if (decide && x_ok) {
-                if (tid < D) {
-                    const int j = tid;
-                    float acc = 0.0f;
-                    for (int i = 0; i <= j; ++i) acc = fmaf(sn[D + packed(i, j)], s_x[i], acc);
-                    s_v[j] = acc;
-                }
-                __syncthreads();
-                if (tid == 0) {
-                    float m = 0.0f, w2 = 0.0f;
-                    for (int i = 0; i < D; ++i) m = fmaf(sn[i], s_x[i], m);
-                    for (int j = 0; j < D; ++j) w2 = fmaf(s_v[j], s_v[j], w2);
-                    s_scal[2] = m;
-                    s_scal[3] = w2;
-                }
-            }
-            __syncthreads();
-        } else if (tid == 0) {
-            p.bad[inst] += 1;
         }
+    } else if (has_prev && tid == 0) {
+        p.bad[inst] += 1;
     }
 
     if (!decide) {
@@ -302,9 +356,9 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
     if (!x_ok) {
         if (p.scores != nullptr) {
             float *sc = p.scores + (size_t)inst * 2 * K;
-            for (int k = tid; k < K; k += nthr) {
-                sc[k] = -INFINITY;
-                sc[K + k] = -INFINITY;
+            for (int q = tid; q < K; q += nthr) {
+                sc[q] = -INFINITY;
+                sc[K + q] = -INFINITY;
             }
         }
         if (tid == 0) {
@@ -319,20 +373,6 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
         return;
     }
 
-    // ---- phase 2: score every active arm (Eq. 1) ----
-    const int k = tid;
-    const uint32_t *mask = p.mask + (size_t)inst * p.KW;
-    const bool active = k < K && ((mask[k >> 5] >> (k & 31)) & 1u);
-    float m = 0.0f, w2 = 0.0f;
-    if (active && k != a_upd) {
-        const float4 *src = p.arms + rec_base + k;
-        const size_t stride = (size_t)K;
-        score_record<D>([&](int c) { return src[(size_t)c * stride]; }, x, m, w2);
-    }
-    if (k == a_upd) {
-        m = s_scal[2];
-        w2 = s_scal[3];
-    }
     float ucb = -INFINITY, lcb = -INFINITY;
     if (active) {
         const float w = sqrtf(fmaxf(w2, 0.0f));
@@ -345,7 +385,7 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
         sc[K + k] = lcb;
     }
 
-    // ---- phase 3: pruning and argmax ----
+    // ---- pruning and argmax ----
     bool keep = active;
     if (p.prune_now) {
         float l = active ? lcb : -INFINITY;
