@@ -82,15 +82,17 @@ typedef struct agft_state_view {
                            followed by S packed by columns, upper part only:
                            S_00, S_01, S_11, S_02, S_12, S_22, ... */
     uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k active */
-    float *xprev;       /* [B][d]: context of the last decision */
-    int32_t *aprev;     /* [B]: last decision, -1 when there is none */
-    int32_t *kact;      /* [B]: number of active arms */
+    int32_t *inst;      /* [B][inst_words] per-instance block of 32-bit words:
+                           [0] last decision (-1: none), [1] number of active arms,
+                           [2] non-finite contexts or rewards met, [3] reserved,
+                           [4 .. 4+d) context of the last decision (fp32) */
+    int32_t inst_words; /* words per instance block: 4 + d rounded up to 16 */
     int32_t *nsel;      /* [B][K]: updates applied to each arm */
-    int32_t *bad;       /* [B]: non-finite contexts or rewards met */
 } agft_state_view;
 
-/* Bytes of device state for cfg (a 256-byte header, then the regions listed
- * in agft_state_view, each 256-byte aligned); 0 if cfg is invalid. */
+/* Bytes of device state for cfg (a 256-byte header, then the arm records,
+ * the masks, the instance blocks and the update counts of agft_state_view,
+ * each region 256-byte aligned); 0 if cfg is invalid. */
 size_t agft_state_bytes(const agft_config *cfg);
 
 /*

@@ -30,7 +30,7 @@ class agft_config(ctypes.Structure):
 class agft_state_view(ctypes.Structure):
     _fields_ = [("t", _i64), ("pending", _i32), ("B", _i32), ("K", _i32), ("d", _i32),
                 ("chunks", _i32), ("mask_words", _i32), ("arms", _vp), ("mask", _vp),
-                ("xprev", _vp), ("aprev", _vp), ("kact", _vp), ("nsel", _vp), ("bad", _vp)]
+                ("inst", _vp), ("inst_words", _i32), ("nsel", _vp)]
 
 
 class agft_env_config(ctypes.Structure):

@@ -66,8 +66,15 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 int chunks_for(int d) { return d / 4 + d * (d + 1) / 8; }
 
+// Per-instance block of 32-bit words: previous action, active-arm count,
+// non-finite-input count, a spare word, then the stashed context.  Kept
+// together so the epilogue writes one or two lines per instance.
+constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstX = 4;
+
+int inst_words(int d) { return (kInstX + d + 15) / 16 * 16; }
+
 struct Layout {
-    size_t arms, mask, xprev, aprev, kact, nsel, bad, total;
+    size_t arms, mask, inst, nsel, total;
 };
 
 Layout layout_for(int B, int K, int d) {
@@ -77,11 +84,8 @@ Layout layout_for(int B, int K, int d) {
     size_t off = sizeof(StateHeader);
     L.arms = off;  off = align_up(off + b * (size_t)chunks_for(d) * k * 16);
     L.mask = off;  off = align_up(off + b * kw * 4);
-    L.xprev = off; off = align_up(off + b * (size_t)d * 4);
-    L.aprev = off; off = align_up(off + b * 4);
-    L.kact = off;  off = align_up(off + b * 4);
+    L.inst = off;  off = align_up(off + b * (size_t)inst_words(d) * 4);
     L.nsel = off;  off = align_up(off + b * k * 4);
-    L.bad = off;   off = align_up(off + b * 4);
     L.total = off;
     return L;
 }
@@ -146,17 +150,14 @@ __device__ __forceinline__ void score_record(Get get, const float *x, float &m, 
 struct StepArgs {
     float4 *arms;
     uint32_t *mask;
-    float *xprev;
-    int32_t *aprev;
-    int32_t *kact;
+    int32_t *inst;        // [B][IW] per-instance blocks
     int32_t *nsel;
-    int32_t *bad;
     StateHeader *hdr;
     const float *ctx;     // [B][D] or nullptr (flush)
     const float *reward;  // [B] or nullptr
     int32_t *action;      // [B] or nullptr
     float *scores;        // [B][2][K] or nullptr
-    int32_t B, K, KW;
+    int32_t B, K, KW, IW;
     int32_t apply_update;  // a decision is pending
     int32_t prune_now;
     float alpha;
@@ -171,6 +172,18 @@ __device__ __forceinline__ float4 ld_nt(const float4 *p) {
     return make_float4(v.x, v.y, v.z, v.w);
 }
 
+// Element `lane` of a register array indexed by a lane-varying value
+// (an unrolled select, so the array stays in registers).
+template <int D>
+__device__ __forceinline__ float x_lane(const float *v, int lane) {
+    float out = 0.0f;
+#pragma unroll
+    for (int q = 0; q < D; ++q) out = (lane == q) ? v[q] : out;
+    return out;
+}
+template <int D>
+__device__ __forceinline__ float xp_lane(const float *v, int lane) { return x_lane<D>(v, lane); }
+
 struct BestPair {
     float v;
     int k;
@@ -184,33 +197,30 @@ __device__ inline BestPair better(BestPair a, BestPair b) {
 template <int D>
 __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
     using R = Rec<D>;
-    // chunks of the updated record each thread loads (workgroups have >= 64 threads)
-    constexpr int NQ = (R::C + kWave - 1) / kWave;
     const int inst = blockIdx.x;
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;
     const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int nwave = nthr / kWave;
     const int K = p.K;
     const size_t rec_base = (size_t)inst * R::C * (size_t)K;
 
     __shared__ float4 s_old[R::C];
     __shared__ float4 s_new[R::C];
-    __shared__ float s_xp[D];
-    __shared__ float s_x[D];
     __shared__ float s_f[D];
     __shared__ float s_ca[D];
     __shared__ float s_cb[D];
     __shared__ float s_scal[4];   // alpha_{d-1}, prediction error, m_a, w2_a
-    __shared__ float s_v[D];
     __shared__ float s_red_v[kMaxWaves];
     __shared__ int s_red_k[kMaxWaves];
     __shared__ int s_red_n[kMaxWaves];
 
     const bool decide = p.ctx != nullptr;
 
-    // Context of this decision: uniform across the workgroup.
+    // Per-instance words, uniform over the workgroup (scalar loads issued
+    // together at kernel start): context, this wavefront's mask words,
+    // previous decision, its reward and its context.
     float x[D];
     bool x_ok = decide;
     if (decide) {
@@ -224,130 +234,132 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
 #pragma unroll
         for (int q = 0; q < D; ++q) x[q] = 0.0f;
     }
-
-    // Pending update of the previous decision's arm.  Its record and the
-    // stashed context are fetched first and consumed after the other arms
-    // have streamed, so their latency overlaps the stream.
-    const int a_prev = p.apply_update ? p.aprev[inst] : -1;
+    const uint32_t *mw = p.mask + (size_t)inst * p.KW;
+    const uint32_t m_lo = 2 * wave < p.KW ? mw[2 * wave] : 0u;
+    const uint32_t m_hi = 2 * wave + 1 < p.KW ? mw[2 * wave + 1] : 0u;
+    int32_t *blk = p.inst + (size_t)inst * p.IW;
+    const int a_prev = p.apply_update ? blk[kInstAprev] : -1;
     const bool has_prev = a_prev >= 0 && a_prev < K;
     const float r = has_prev ? p.reward[inst] : 0.0f;
     const bool upd = has_prev && isfinite(r);
     const int a_upd = upd ? a_prev : -1;
-    float4 old_chunk[NQ];
-    float xp_val = 0.0f;
+    float xp[D];
+    if (upd) {
+        const float *xpi = reinterpret_cast<const float *>(blk + kInstX);
+#pragma unroll
+        for (int q = 0; q < D; ++q) xp[q] = xpi[q];
+    }
+
+    // ---- scoring of every active arm (Eq. 1) ----
+    // The lane of the previous decision's arm also leaves that arm's record
+    // in LDS for the update below; its own score is replaced afterwards.
+    const int k = tid;
+    const bool active = k < K && (((lane < 32 ? m_lo >> lane : m_hi >> (lane - 32)) & 1u) != 0);
+    float m = 0.0f, w2 = 0.0f;
+    float4 old_chunk[(R::C + kWave - 1) / kWave];
     if (upd) {
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
+        for (int q = 0; q < (R::C + kWave - 1) / kWave; ++q) {
             const int c = tid + q * nthr;
             if (c < R::C) old_chunk[q] = p.arms[rec_base + (size_t)c * K + a_upd];
         }
-        if (tid < D) xp_val = p.xprev[(size_t)inst * D + tid];
     }
-
-    // ---- scoring of every other active arm (Eq. 1) ----
-    const int k = tid;
-    const uint32_t *mask = p.mask + (size_t)inst * p.KW;
-    const bool active = x_ok && k < K && ((mask[k >> 5] >> (k & 31)) & 1u);
-    float m = 0.0f, w2 = 0.0f;
-    if (active && k != a_upd) {
+    if (x_ok && active && k != a_upd) {
         const float4 *src = p.arms + rec_base + k;
         const size_t stride = (size_t)K;
         score_record<D>([&](int c) { return ld_nt(&src[(size_t)c * stride]); }, x, m, w2);
     }
-
-    // ---- square-root rank-1 update of the previous decision's arm ----
     if (upd) {
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) {
+        for (int q = 0; q < (R::C + kWave - 1) / kWave; ++q) {
             const int c = tid + q * nthr;
             if (c < R::C) s_old[c] = old_chunk[q];
         }
-        if (tid < D) {
-            s_xp[tid] = xp_val;
-            s_x[tid] = x[tid];
-        }
+    }
+
+    // ---- square-root rank-1 update of the previous decision's arm ----
+    if (upd) {
         __syncthreads();
         const float *so = reinterpret_cast<const float *>(s_old);
         const float *sth = so;             // theta
         const float *sS = so + D;          // packed factor
-        if (tid < D) {
-            // f_j = sum_{i<=j} S_ij xp_i
-            const int j = tid;
-            float acc = 0.0f;
-            for (int i = 0; i <= j; ++i) acc = fmaf(sS[packed(i, j)], s_xp[i], acc);
-            s_f[j] = acc;
-        }
-        __syncthreads();
-        if (tid < kWave) {
-            // alpha_j = 1 + f_0^2 + ... + f_j^2 by a wavefront scan, the
-            // column coefficients, and the prediction error r - xp^T theta
-            const float fj = tid < D ? s_f[tid] : 0.0f;
+        float *sn = reinterpret_cast<float *>(s_new);
+        if (wave == 0) {
+            // f_j = sum_{i<=j} S_ij xp_i, alpha_j = 1 + f_0^2 + ... + f_j^2 (scan),
+            // column coefficients, prediction error r - xp^T theta
+            float fj = 0.0f;
+#pragma unroll
+            for (int i = 0; i < D; ++i)
+                if (i <= lane) fj = fmaf(sS[packed(i, lane < D ? lane : 0)], xp[i], fj);
+            if (lane >= D) fj = 0.0f;
             float incl = fj * fj;
 #pragma unroll
             for (int off = 1; off < D; off <<= 1) {
                 const float y = __shfl_up(incl, off);
                 if (lane >= off) incl += y;
             }
-            float pred = tid < D ? s_xp[tid] * sth[tid] : 0.0f;
+            float pred = lane < D ? xp_lane<D>(xp, lane) * sth[lane < D ? lane : 0] : 0.0f;
 #pragma unroll
             for (int off = kWave / 2; off > 0; off >>= 1) pred += __shfl_xor(pred, off);
-            if (tid < D) {
+            if (lane < D) {
                 const float al = 1.0f + incl;
                 const float al_prev = 1.0f + (incl - fj * fj);
-                s_ca[tid] = sqrtf(al_prev / al);
-                s_cb[tid] = fj / sqrtf(al_prev * al);
-                if (tid == D - 1) s_scal[0] = al;
+                s_f[lane] = fj;
+                s_ca[lane] = sqrtf(al_prev / al);
+                s_cb[lane] = fj / sqrtf(al_prev * al);
+                if (lane == D - 1) s_scal[0] = al;
             }
-            if (tid == 0) s_scal[1] = r - pred;
+            if (lane == 0) s_scal[1] = r - pred;
         }
         __syncthreads();
-        float *sn = reinterpret_cast<float *>(s_new);
-        for (int e = tid; e < R::NSE; e += nthr) {
-            int i, j;
-            unpack(e, i, j);
+        if (wave == 0 && lane < D) {
+            // row i of S' = S M:  S'_ij = ca_j S_ij - cb_j g,  g = sum_{i<=q<j} f_q S_iq;
+            // the final g is (S f)_i, so the gain is g / alpha_{d-1}
+            const int i = lane;
             float g = 0.0f;
-            for (int q = i; q < j; ++q) g = fmaf(s_f[q], sS[packed(i, q)], g);
-            sn[D + e] = s_ca[j] * sS[e] - s_cb[j] * g;
-        }
-        if (tid < D) {
-            // gain g_i = (S f)_i / alpha_{d-1}
-            const int i = tid;
-            float sf = 0.0f;
-            for (int q = i; q < D; ++q) sf = fmaf(sS[packed(i, q)], s_f[q], sf);
-            sn[i] = fmaf(sf / s_scal[0], s_scal[1], sth[i]);
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                if (j >= i) {
+                    const float sij = sS[packed(i, j)];
+                    sn[D + packed(i, j)] = s_ca[j] * sij - s_cb[j] * g;
+                    g = fmaf(s_f[j], sij, g);
+                }
+            }
+            sn[i] = fmaf(g / s_scal[0], s_scal[1], sth[i]);
         }
         __syncthreads();
         for (int c = tid; c < R::C; c += nthr) p.arms[rec_base + (size_t)c * K + a_upd] = s_new[c];
         if (tid == 0) p.nsel[(size_t)inst * K + a_upd] += 1;
-        if (x_ok) {
+        if (x_ok && wave == 0) {
             // score the updated arm on x_t from LDS, in the streaming order
-            if (tid < D) {
-                const int j = tid;
-                float acc = 0.0f;
-                for (int i = 0; i <= j; ++i) acc = fmaf(sn[D + packed(i, j)], s_x[i], acc);
-                s_v[j] = acc;
+            float vj = 0.0f;
+#pragma unroll
+            for (int i = 0; i < D; ++i)
+                if (i <= lane) vj = fmaf(sn[D + packed(i, lane < D ? lane : 0)], x[i], vj);
+            float ma = 0.0f, w2a = 0.0f;
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                const float v = __shfl(vj, j);
+                w2a = fmaf(v, v, w2a);
+                ma = fmaf(sn[j], x[j], ma);
             }
-            __syncthreads();
-            if (tid == 0) {
-                float ma = 0.0f, w2a = 0.0f;
-                for (int i = 0; i < D; ++i) ma = fmaf(sn[i], s_x[i], ma);
-                for (int j = 0; j < D; ++j) w2a = fmaf(s_v[j], s_v[j], w2a);
+            if (lane == 0) {
                 s_scal[2] = ma;
                 s_scal[3] = w2a;
             }
-            __syncthreads();
-            if (k == a_upd) {
-                m = s_scal[2];
-                w2 = s_scal[3];
-            }
+        }
+        __syncthreads();
+        if (x_ok && k == a_upd) {
+            m = s_scal[2];
+            w2 = s_scal[3];
         }
     } else if (has_prev && tid == 0) {
-        p.bad[inst] += 1;
+        blk[kInstBad] += 1;
     }
 
     if (!decide) {
         if (tid == 0) {
-            p.aprev[inst] = -1;
+            blk[kInstAprev] = -1;
             if (inst == 0) p.hdr->pending = 0;
         }
         return;
@@ -362,8 +374,8 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
             }
         }
         if (tid == 0) {
-            p.bad[inst] += 1;
-            p.aprev[inst] = -1;
+            blk[kInstBad] += 1;
+            blk[kInstAprev] = -1;
             if (p.action != nullptr) p.action[inst] = -1;
             if (inst == 0) {
                 p.hdr->t = p.t_next;
@@ -399,10 +411,10 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
     }
     const unsigned long long bal = __ballot(keep);
     if (p.prune_now) {
-        uint32_t *mw = p.mask + (size_t)inst * p.KW;
+        uint32_t *mwo = p.mask + (size_t)inst * p.KW;
         const int w0 = 2 * wave;
-        if (lane == 0 && w0 < p.KW) mw[w0] = (uint32_t)(bal & 0xffffffffull);
-        if (lane == 0 && w0 + 1 < p.KW) mw[w0 + 1] = (uint32_t)(bal >> 32);
+        if (lane == 0 && w0 < p.KW) mwo[w0] = (uint32_t)(bal & 0xffffffffull);
+        if (lane == 0 && w0 + 1 < p.KW) mwo[w0 + 1] = (uint32_t)(bal >> 32);
     }
     BestPair b{keep ? ucb : -INFINITY, keep ? k : 0x7fffffff};
     for (int off = kWave / 2; off > 0; off >>= 1) {
@@ -415,7 +427,9 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
         s_red_n[wave] = __popcll(bal);
     }
     __syncthreads();
-    if (tid == 0) {
+    if (wave == 0) {
+        // every lane of wavefront 0 reduces the per-wave results, then the
+        // lanes write the instance block (action, count, context) at once
         BestPair best{s_red_v[0], s_red_k[0]};
         int n = s_red_n[0];
         for (int w = 1; w < nwave; ++w) {
@@ -423,15 +437,18 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
             n += s_red_n[w];
         }
         const int a = best.k == 0x7fffffff ? -1 : best.k;
-        if (p.action != nullptr) p.action[inst] = a;
-        p.aprev[inst] = a;
-        p.kact[inst] = n;
-        if (inst == 0) {
-            p.hdr->t = p.t_next;
-            p.hdr->pending = 1;
+        if (lane == 0) {
+            if (p.action != nullptr) p.action[inst] = a;
+            if (inst == 0) {
+                p.hdr->t = p.t_next;
+                p.hdr->pending = 1;
+            }
         }
+        if (lane == kInstAprev) blk[kInstAprev] = a;
+        if (lane == kInstKact) blk[kInstKact] = n;
+        if (lane >= kInstX && lane < kInstX + D)
+            reinterpret_cast<float *>(blk)[lane] = x_lane<D>(x, lane - kInstX);
     }
-    if (tid < D) p.xprev[(size_t)inst * D + tid] = x[tid];
 }
 
 // ---- initialisation and export ----
@@ -439,14 +456,11 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
 struct InitArgs {
     float4 *arms;
     uint32_t *mask;
-    float *xprev;
-    int32_t *aprev;
-    int32_t *kact;
+    int32_t *inst;
     int32_t *nsel;
-    int32_t *bad;
     StateHeader *hdr;
     StateHeader h;
-    int32_t B, K, KW, d, C;
+    int32_t B, K, KW, d, C, IW;
     float inv_sqrt_lambda;
 };
 
@@ -473,12 +487,10 @@ __global__ void agft_init_kernel(InitArgs p) {
         const int rem = p.K - 32 * w;
         p.mask[idx] = rem >= 32 ? 0xffffffffu : ((1u << rem) - 1u);
     }
-    for (size_t idx = gtid; idx < (size_t)p.B * p.d; idx += gsz) p.xprev[idx] = 0.0f;
     for (size_t idx = gtid; idx < (size_t)p.B * p.K; idx += gsz) p.nsel[idx] = 0;
-    for (size_t idx = gtid; idx < (size_t)p.B; idx += gsz) {
-        p.aprev[idx] = -1;
-        p.kact[idx] = p.K;
-        p.bad[idx] = 0;
+    for (size_t idx = gtid; idx < (size_t)p.B * p.IW; idx += gsz) {
+        const int w = (int)(idx % p.IW);
+        p.inst[idx] = w == kInstAprev ? -1 : (w == kInstKact ? p.K : 0);
     }
     if (gtid == 0) *p.hdr = p.h;
 }
@@ -615,11 +627,8 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     InitArgs a;
     a.arms = at<float4>(h->base, lay.arms);
     a.mask = at<uint32_t>(h->base, lay.mask);
-    a.xprev = at<float>(h->base, lay.xprev);
-    a.aprev = at<int32_t>(h->base, lay.aprev);
-    a.kact = at<int32_t>(h->base, lay.kact);
+    a.inst = at<int32_t>(h->base, lay.inst);
     a.nsel = at<int32_t>(h->base, lay.nsel);
-    a.bad = at<int32_t>(h->base, lay.bad);
     a.hdr = at<StateHeader>(h->base, 0);
     a.h = want;
     a.B = cfg->B;
@@ -627,6 +636,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     a.KW = (cfg->K + 31) / 32;
     a.d = cfg->d;
     a.C = chunks_for(cfg->d);
+    a.IW = inst_words(cfg->d);
     a.inv_sqrt_lambda = (float)(1.0 / std::sqrt((double)cfg->lambda));
     const size_t work = (size_t)cfg->B * a.C * cfg->K;
     size_t blocks = (work + 255) / 256;
@@ -649,11 +659,8 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     StepArgs p;
     p.arms = at<float4>(h->base, h->lay.arms);
     p.mask = at<uint32_t>(h->base, h->lay.mask);
-    p.xprev = at<float>(h->base, h->lay.xprev);
-    p.aprev = at<int32_t>(h->base, h->lay.aprev);
-    p.kact = at<int32_t>(h->base, h->lay.kact);
+    p.inst = at<int32_t>(h->base, h->lay.inst);
     p.nsel = at<int32_t>(h->base, h->lay.nsel);
-    p.bad = at<int32_t>(h->base, h->lay.bad);
     p.hdr = at<StateHeader>(h->base, 0);
     p.ctx = d_ctx;
     p.reward = d_reward;
@@ -662,6 +669,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.B = c.B;
     p.K = c.K;
     p.KW = (c.K + 31) / 32;
+    p.IW = inst_words(c.d);
     p.apply_update = h->pending;
     const int64_t t = h->t;
     p.prune_now = (d_ctx != nullptr && c.prune_rule == 1 && t > 0 && t % c.prune_period == 0) ? 1 : 0;
@@ -697,11 +705,9 @@ int agft_get_state(const agft_handle *h, agft_state_view *out) {
     out->mask_words = (h->cfg.K + 31) / 32;
     out->arms = h->base + h->lay.arms;
     out->mask = at<uint32_t>(h->base, h->lay.mask);
-    out->xprev = at<float>(h->base, h->lay.xprev);
-    out->aprev = at<int32_t>(h->base, h->lay.aprev);
-    out->kact = at<int32_t>(h->base, h->lay.kact);
+    out->inst = at<int32_t>(h->base, h->lay.inst);
+    out->inst_words = inst_words(h->cfg.d);
     out->nsel = at<int32_t>(h->base, h->lay.nsel);
-    out->bad = at<int32_t>(h->base, h->lay.bad);
     return AGFT_OK;
 }
 

@@ -102,16 +102,16 @@ class Tuner:
             nb = count * torch.tensor([], dtype=dtype).element_size()
             return self.state[off:off + nb].view(dtype).view(shape)
 
-        B, K, d, C, KW = v.B, v.K, v.d, v.chunks, v.mask_words
+        B, K, d, C, KW, IW = v.B, v.K, v.d, v.chunks, v.mask_words, v.inst_words
+        inst = region(v.inst, B * IW, torch.int32, (B, IW))
         return dict(
             t=int(v.t), pending=int(v.pending),
             arms=region(v.arms, B * C * K * 4, torch.float32, (B, C, K, 4)),
             mask=region(v.mask, B * KW, torch.int32, (B, KW)),
-            xprev=region(v.xprev, B * d, torch.float32, (B, d)),
-            aprev=region(v.aprev, B, torch.int32, (B,)),
-            kact=region(v.kact, B, torch.int32, (B,)),
+            inst=inst,
+            aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2],
+            xprev=inst[:, 4:4 + d].view(torch.float32),
             nsel=region(v.nsel, B * K, torch.int32, (B, K)),
-            bad=region(v.bad, B, torch.int32, (B,)),
         )
 
     @property
