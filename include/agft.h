@@ -75,12 +75,17 @@ typedef struct agft_state_view {
     int64_t t;          /* decisions made so far */
     int32_t pending;    /* 1 while the last decision awaits its reward */
     int32_t B, K, d;
-    int32_t chunks;     /* float4 chunks per arm record: d/4 + d(d+1)/8 */
+    int32_t chunks;     /* float4 chunks per arm record: (d/2) * ((d+6)/4) */
     int32_t mask_words; /* uint32 words per instance in the action-set mask: ceil(K/32) */
-    void *arms;         /* float4 [B][chunks][K]: chunk c of arm k of instance i at
-                           index (i*chunks + c)*K + k.  A record is theta_0..theta_{d-1}
-                           followed by S packed by columns, upper part only:
-                           S_00, S_01, S_11, S_02, S_12, S_22, ... */
+    void *arms;         /* float4 [B][K][chunks]: arm k of instance i is the contiguous
+                           record at index (i*K + k)*chunks.  A record is split into
+                           G = d/2 lane slices of (d+6)/4 chunks; chunk s*G + j holds
+                           positions 4s..4s+3 of slice j, whose positions are
+                             e = 0..j:      S_{e,j}            (column j of S)
+                             e = j+1..d:    S_{d-e, d-1-j}     (column d-1-j, bottom up)
+                             e = d+1, d+2:  theta_{2j}, theta_{2j+1}
+                             e > d+2:       0
+                           with S upper triangular, S S^T = A^{-1}. */
     uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k active */
     int32_t *inst;      /* [B][inst_words] per-instance block of 32-bit words:
                            [0] last decision (-1: none), [1] number of active arms,

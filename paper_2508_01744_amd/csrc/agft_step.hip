@@ -1,16 +1,20 @@
 // agft_step.hip -- batched AGFT decide-and-update step for CDNA4 (gfx950).
 //
-// One workgroup per tuner instance, one lane per frequency arm: lane k of the
-// workgroup streams arm k's record (theta_k and the packed factor S_k of
-// A_k^{-1}) from HBM and scores it without any cross-lane traffic, because
-// the context x_t is uniform over the workgroup and lives in scalar
-// registers.  Records are interleaved across arms in 16-byte chunks, so for
-// every chunk index the 64 lanes of a wavefront read 1 KiB of contiguous
-// memory.
+// One workgroup per tuner instance.  Each arm's record (theta_k and the
+// packed upper factor S_k of A_k^{-1}) is contiguous in HBM and is read by a
+// group of G = d/2 lanes: lane j of the group owns factor columns j and
+// d-1-j (d+1 elements together) and theta_{2j}, theta_{2j+1}, so it forms
+// two complete entries of v = S^T x_t and two terms of theta^T x_t on its
+// own, and the group only sums two numbers at the end.  For every load
+// instruction the G lanes of a group read G x 16 contiguous bytes of one
+// record and a wavefront covers whole cache lines.  Keeping a record
+// contiguous matters for the update: rewriting one arm touches a handful of
+// cache lines instead of one line per 16-byte piece.
 //
 // Per step and instance (Sec. 4.2):
-//   1. fetch the record of the previous decision's arm (its update waits);
-//   2. every other active arm: v = S^T x_t, w^2 = |v|^2, m = theta^T x_t,
+//   1. fetch the record of the previous decision's arm (its update waits)
+//      and list the other active arms (the list skips pruned arms);
+//   2. every listed arm: m = theta^T x_t, w^2 = |S^T x_t|^2,
 //      UCB = m + alpha_t w, LCB = m - alpha_t w  (Eq. 1);
 //   3. fold the previous decision's reward into its arm: Eq. 3-5 as a
 //      square-root rank-1 update of S (below) plus the matching theta
@@ -47,7 +51,8 @@ namespace {
 constexpr uint32_t kMagic = 0x54464741u;  // "AGFT"
 constexpr int kWave = 64;
 constexpr int kMaxK = 1024;
-constexpr int kMaxWaves = kMaxK / kWave;
+constexpr int kMaxWords = kMaxK / 32;
+constexpr int kMaxWaves = 16;
 constexpr size_t kAlign = 256;
 
 // Header at the start of the state buffer (256 bytes).
@@ -64,7 +69,40 @@ static_assert(sizeof(StateHeader) == 256, "header is 256 bytes");
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
-int chunks_for(int d) { return d / 4 + d * (d + 1) / 8; }
+// Record geometry for context dimension D: G lanes per arm, each owning
+// P = D + 1 factor elements and two theta entries, padded to S float4 chunks.
+template <int D>
+struct Rec {
+    static constexpr int G = D / 2;              // lanes per arm
+    static constexpr int P = D + 1;              // factor elements per lane
+    static constexpr int S = (D + 3 + 3) / 4;    // chunks per lane
+    static constexpr int R = G * S;              // chunks per record
+    static constexpr int NSE = D * (D + 1) / 2;  // packed factor elements
+    static constexpr int CAN = D + NSE;          // canonical floats: theta, then packed S
+};
+
+int chunks_for(int d) { return (d / 2) * ((d + 6) / 4); }
+
+// Packed column-major index of S_ij (i <= j) within the factor part.
+__host__ __device__ constexpr int packed(int i, int j) { return j * (j + 1) / 2 + i; }
+
+// Canonical index (theta_0..theta_{D-1}, then packed S) of position e of
+// lane j's slice of a record; -1 for padding.
+__host__ __device__ constexpr int canon(int D, int j, int e) {
+    return e <= j ? D + packed(e, j)
+         : e <= D ? D + packed(D - e, D - 1 - j)
+         : e == D + 1 ? 2 * j
+         : e == D + 2 ? 2 * j + 1
+         : -1;
+}
+
+// Column j and row i of packed element e.
+__device__ inline void unpack(int e, int &i, int &j) {
+    int c = 0;
+    while ((c + 1) * (c + 2) / 2 <= e) ++c;
+    j = c;
+    i = e - c * (c + 1) / 2;
+}
 
 // Per-instance block of 32-bit words: previous action, active-arm count,
 // non-finite-input count, a spare word, then the stashed context.  Kept
@@ -82,7 +120,7 @@ Layout layout_for(int B, int K, int d) {
     const size_t b = (size_t)B, k = (size_t)K;
     const size_t kw = (k + 31) / 32;
     size_t off = sizeof(StateHeader);
-    L.arms = off;  off = align_up(off + b * (size_t)chunks_for(d) * k * 16);
+    L.arms = off;  off = align_up(off + b * k * (size_t)chunks_for(d) * 16);
     L.mask = off;  off = align_up(off + b * kw * 4);
     L.inst = off;  off = align_up(off + b * (size_t)inst_words(d) * 4);
     L.nsel = off;  off = align_up(off + b * k * 4);
@@ -90,61 +128,36 @@ Layout layout_for(int B, int K, int d) {
     return L;
 }
 
-// Record geometry for context dimension D.
-template <int D>
-struct Rec {
-    static constexpr int NT = D / 4;             // theta chunks
-    static constexpr int NSE = D * (D + 1) / 2;  // packed factor elements
-    static constexpr int NS = NSE / 4;           // factor chunks
-    static constexpr int C = NT + NS;            // chunks per record
-    static constexpr int F = 4 * C;              // floats per record
-    static_assert(NSE % 4 == 0, "packed factor fills whole chunks");
-};
-
-// Packed column-major index of S_ij (i <= j) within the factor part.
-__host__ __device__ constexpr int packed(int i, int j) { return j * (j + 1) / 2 + i; }
-
-// Column j and row i of packed element e.
-__device__ inline void unpack(int e, int &i, int &j) {
-    int c = 0;
-    while ((c + 1) * (c + 2) / 2 <= e) ++c;
-    j = c;
-    i = e - c * (c + 1) / 2;
+// Workgroup width for K arms of dimension d: enough groups of d/2 lanes for
+// all arms, at most 4 wavefronts (larger K loops over the arms).
+int waves_for(int K, int d) {
+    const int lanes = K * (d / 2);
+    int w = (lanes + kWave - 1) / kWave;
+    return w < 1 ? 1 : (w > 4 ? 4 : w);
 }
 
-// Eq. 1 ingredients of one arm record: m = theta^T x and w2 = |S^T x|^2.
-// get(c) yields chunk c of the record; the operation order is fixed so the
-// streaming path and the LDS path give bit-identical results on equal data.
-template <int D, class Get>
-__device__ __forceinline__ void score_record(Get get, const float *x, float &m, float &w2) {
-    m = 0.0f;
+// Per-lane slice of the Eq. 1 terms from the S chunks of one record slice:
+// va, vb = the two owned entries of S^T x, m = the two owned theta terms.
+// xa/xb hold x_e (e <= j) and x_{D-e} (e > j) for this lane's positions.
+template <int D>
+__device__ __forceinline__ void slice_terms(const float *f, const float *xa, const float *xb,
+                                            float xt0, float xt1, float &m, float &w2) {
+    float va = 0.0f, vb = 0.0f;
 #pragma unroll
-    for (int c = 0; c < Rec<D>::NT; ++c) {
-        const float4 v = get(c);
-        m = fmaf(v.x, x[4 * c + 0], m);
-        m = fmaf(v.y, x[4 * c + 1], m);
-        m = fmaf(v.z, x[4 * c + 2], m);
-        m = fmaf(v.w, x[4 * c + 3], m);
+    for (int e = 0; e <= D; ++e) {
+        va = fmaf(f[e], xa[e], va);
+        vb = fmaf(f[e], xb[e], vb);
     }
-    w2 = 0.0f;
-    float acc = 0.0f;
-    int i = 0, j = 0;
+    m = fmaf(f[D + 2], xt1, f[D + 1] * xt0);
+    w2 = fmaf(vb, vb, va * va);
+}
+
+// Sum over the G lanes of a group (butterfly: every lane ends with the total).
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
 #pragma unroll
-    for (int c = 0; c < Rec<D>::NS; ++c) {
-        const float4 v = get(Rec<D>::NT + c);
-        const float e[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            acc = fmaf(e[q], x[i], i == 0 ? 0.0f : acc);
-            if (i == j) {
-                w2 = fmaf(acc, acc, w2);
-                ++j;
-                i = 0;
-            } else {
-                ++i;
-            }
-        }
-    }
+    for (int off = G / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
 }
 
 struct StepArgs {
@@ -172,17 +185,15 @@ __device__ __forceinline__ float4 ld_nt(const float4 *p) {
     return make_float4(v.x, v.y, v.z, v.w);
 }
 
-// Element `lane` of a register array indexed by a lane-varying value
+// Element `idx` of a register array indexed by a lane-varying value
 // (an unrolled select, so the array stays in registers).
-template <int D>
-__device__ __forceinline__ float x_lane(const float *v, int lane) {
+template <int N>
+__device__ __forceinline__ float pick(const float *v, int idx) {
     float out = 0.0f;
 #pragma unroll
-    for (int q = 0; q < D; ++q) out = (lane == q) ? v[q] : out;
+    for (int q = 0; q < N; ++q) out = (idx == q) ? v[q] : out;
     return out;
 }
-template <int D>
-__device__ __forceinline__ float xp_lane(const float *v, int lane) { return x_lane<D>(v, lane); }
 
 struct BestPair {
     float v;
@@ -195,8 +206,10 @@ __device__ inline BestPair better(BestPair a, BestPair b) {
 }
 
 template <int D>
-__global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
+__global__ __launch_bounds__(256) void agft_step_kernel(StepArgs p) {
     using R = Rec<D>;
+    constexpr int G = R::G, S = R::S;
+    constexpr int NQ = (R::R + kWave - 1) / kWave;   // update-record chunks per thread (>= 64 threads)
     const int inst = blockIdx.x;
     const int tid = threadIdx.x;
     const int nthr = blockDim.x;
@@ -204,23 +217,31 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
     const int nwave = nthr / kWave;
     const int K = p.K;
-    const size_t rec_base = (size_t)inst * R::C * (size_t)K;
+    const int KW = p.KW;
+    const int j = tid % G;           // slot of this lane within its arm's group
+    const int grp = tid / G;         // group index within the workgroup
+    const int apw = nthr / G;        // arms per pass of the workgroup
+    const float4 *recs = p.arms + (size_t)inst * K * R::R;
 
-    __shared__ float4 s_old[R::C];
-    __shared__ float4 s_new[R::C];
+    __shared__ float s_old[R::CAN];
+    __shared__ float s_new[R::CAN];
     __shared__ float s_f[D];
     __shared__ float s_ca[D];
     __shared__ float s_cb[D];
-    __shared__ float s_scal[4];   // alpha_{d-1}, prediction error, m_a, w2_a
+    __shared__ float s_scal[2];   // alpha_{d-1}, prediction error
+    __shared__ float s_ucb[kMaxK];
+    __shared__ float s_lcb[kMaxK];
+    __shared__ short s_list[kMaxK];
+    __shared__ uint32_t s_mask[kMaxWords];
+    __shared__ int s_nlist;
     __shared__ float s_red_v[kMaxWaves];
     __shared__ int s_red_k[kMaxWaves];
     __shared__ int s_red_n[kMaxWaves];
 
     const bool decide = p.ctx != nullptr;
 
-    // Per-instance words, uniform over the workgroup (scalar loads issued
-    // together at kernel start): context, this wavefront's mask words,
-    // previous decision, its reward and its context.
+    // Per-instance words, uniform over the workgroup (scalar loads at kernel
+    // start): context, previous decision, its reward and its context.
     float x[D];
     bool x_ok = decide;
     if (decide) {
@@ -234,9 +255,6 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
 #pragma unroll
         for (int q = 0; q < D; ++q) x[q] = 0.0f;
     }
-    const uint32_t *mw = p.mask + (size_t)inst * p.KW;
-    const uint32_t m_lo = 2 * wave < p.KW ? mw[2 * wave] : 0u;
-    const uint32_t m_hi = 2 * wave + 1 < p.KW ? mw[2 * wave + 1] : 0u;
     int32_t *blk = p.inst + (size_t)inst * p.IW;
     const int a_prev = p.apply_update ? blk[kInstAprev] : -1;
     const bool has_prev = a_prev >= 0 && a_prev < K;
@@ -250,40 +268,113 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
         for (int q = 0; q < D; ++q) xp[q] = xpi[q];
     }
 
-    // ---- scoring of every active arm (Eq. 1) ----
-    // The lane of the previous decision's arm also leaves that arm's record
-    // in LDS for the update below; its own score is replaced afterwards.
-    const int k = tid;
-    const bool active = k < K && (((lane < 32 ? m_lo >> lane : m_hi >> (lane - 32)) & 1u) != 0);
-    float m = 0.0f, w2 = 0.0f;
-    float4 old_chunk[(R::C + kWave - 1) / kWave];
+    // Record of the previous decision's arm: fetched now, consumed after the stream.
+    float4 old_chunk[NQ];
     if (upd) {
+        const float4 *src = recs + (size_t)a_upd * R::R;
 #pragma unroll
-        for (int q = 0; q < (R::C + kWave - 1) / kWave; ++q) {
+        for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
-            if (c < R::C) old_chunk[q] = p.arms[rec_base + (size_t)c * K + a_upd];
+            if (c < R::R) old_chunk[q] = src[c];
         }
     }
-    if (x_ok && active && k != a_upd) {
-        const float4 *src = p.arms + rec_base + k;
-        const size_t stride = (size_t)K;
-        score_record<D>([&](int c) { return ld_nt(&src[(size_t)c * stride]); }, x, m, w2);
-    }
-    if (upd) {
+
+    // Active arms other than the one being updated, in index order.
+    if (wave == 0) {
+        const uint32_t w = lane < KW ? p.mask[(size_t)inst * KW + lane] : 0u;
+        if (lane < KW) s_mask[lane] = w;
+        uint32_t wl = w;
+        if (x_ok && a_upd >= 0 && (a_upd >> 5) == lane) wl &= ~(1u << (a_upd & 31));
+        if (!x_ok) wl = 0u;
+        const int cnt = __popc(wl);
+        int incl = cnt;
 #pragma unroll
-        for (int q = 0; q < (R::C + kWave - 1) / kWave; ++q) {
-            const int c = tid + q * nthr;
-            if (c < R::C) s_old[c] = old_chunk[q];
+        for (int off = 1; off < kMaxWords; off <<= 1) {
+            const int y = __shfl_up(incl, off);
+            if (lane >= off) incl += y;
+        }
+        int pos = incl - cnt;
+        while (wl) {
+            const int b = __ffs(wl) - 1;
+            s_list[pos++] = (short)(32 * lane + b);
+            wl &= wl - 1;
+        }
+        if (lane == kMaxWords - 1) s_nlist = incl;
+    }
+
+    // This lane's selectors of x: xa_e = x_e for e <= j, xb_e = x_{D-e} for e > j.
+    float xa[D + 1], xb[D + 1];
+#pragma unroll
+    for (int e = 0; e <= D; ++e) {
+        xa[e] = e <= j ? x[e] : 0.0f;
+        xb[e] = (e > j && e >= 1) ? x[D - e < 0 ? 0 : D - e] : 0.0f;
+    }
+    const float xt0 = pick<D>(x, 2 * j), xt1 = pick<D>(x, 2 * j + 1);
+    __syncthreads();
+
+    // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
+    const int nlist = s_nlist;
+    {
+        float4 cur[S], nxt[S];
+        int k_cur = grp < nlist ? s_list[grp] : -1;
+        if (k_cur >= 0) {
+            const float4 *src = recs + (size_t)k_cur * R::R + j;
+#pragma unroll
+            for (int sidx = 0; sidx < S; ++sidx) cur[sidx] = ld_nt(src + sidx * G);
+        }
+        for (int base = 0; base < nlist; base += apw) {
+            const int slot_n = base + apw + grp;
+            const int k_nxt = slot_n < nlist ? s_list[slot_n] : -1;
+            if (k_nxt >= 0) {
+                const float4 *src = recs + (size_t)k_nxt * R::R + j;
+#pragma unroll
+                for (int sidx = 0; sidx < S; ++sidx) nxt[sidx] = ld_nt(src + sidx * G);
+            }
+            float f[4 * S];
+#pragma unroll
+            for (int sidx = 0; sidx < S; ++sidx) {
+                f[4 * sidx + 0] = cur[sidx].x;
+                f[4 * sidx + 1] = cur[sidx].y;
+                f[4 * sidx + 2] = cur[sidx].z;
+                f[4 * sidx + 3] = cur[sidx].w;
+            }
+            float m, w2;
+            slice_terms<D>(f, xa, xb, xt0, xt1, m, w2);
+            if (k_cur < 0) {
+                m = 0.0f;
+                w2 = 0.0f;
+            }
+            m = group_sum<G>(m);
+            w2 = group_sum<G>(w2);
+            if (k_cur >= 0 && j == 0) {
+                const float w = sqrtf(w2);
+                s_ucb[k_cur] = fmaf(p.alpha, w, m);
+                s_lcb[k_cur] = fmaf(-p.alpha, w, m);
+            }
+#pragma unroll
+            for (int sidx = 0; sidx < S; ++sidx) cur[sidx] = nxt[sidx];
+            k_cur = k_nxt;
         }
     }
 
     // ---- square-root rank-1 update of the previous decision's arm ----
     if (upd) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int c = tid + q * nthr;
+            if (c < R::R) {
+                const int sl = c / G, jj = c % G;
+                const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    const int ci = canon(D, jj, 4 * sl + qq);
+                    if (ci >= 0) s_old[ci] = v[qq];
+                }
+            }
+        }
         __syncthreads();
-        const float *so = reinterpret_cast<const float *>(s_old);
-        const float *sth = so;             // theta
-        const float *sS = so + D;          // packed factor
-        float *sn = reinterpret_cast<float *>(s_new);
+        const float *sth = s_old;         // theta
+        const float *sS = s_old + D;      // packed factor
         if (wave == 0) {
             // f_j = sum_{i<=j} S_ij xp_i, alpha_j = 1 + f_0^2 + ... + f_j^2 (scan),
             // column coefficients, prediction error r - xp^T theta
@@ -298,7 +389,7 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
                 const float y = __shfl_up(incl, off);
                 if (lane >= off) incl += y;
             }
-            float pred = lane < D ? xp_lane<D>(xp, lane) * sth[lane < D ? lane : 0] : 0.0f;
+            float pred = lane < D ? pick<D>(xp, lane) * sth[lane < D ? lane : 0] : 0.0f;
 #pragma unroll
             for (int off = kWave / 2; off > 0; off >>= 1) pred += __shfl_xor(pred, off);
             if (lane < D) {
@@ -318,40 +409,45 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
             const int i = lane;
             float g = 0.0f;
 #pragma unroll
-            for (int j = 0; j < D; ++j) {
-                if (j >= i) {
-                    const float sij = sS[packed(i, j)];
-                    sn[D + packed(i, j)] = s_ca[j] * sij - s_cb[j] * g;
-                    g = fmaf(s_f[j], sij, g);
+            for (int jc = 0; jc < D; ++jc) {
+                if (jc >= i) {
+                    const float sij = sS[packed(i, jc)];
+                    s_new[D + packed(i, jc)] = s_ca[jc] * sij - s_cb[jc] * g;
+                    g = fmaf(s_f[jc], sij, g);
                 }
             }
-            sn[i] = fmaf(g / s_scal[0], s_scal[1], sth[i]);
+            s_new[i] = fmaf(g / s_scal[0], s_scal[1], sth[i]);
         }
         __syncthreads();
-        for (int c = tid; c < R::C; c += nthr) p.arms[rec_base + (size_t)c * K + a_upd] = s_new[c];
+        float4 *dst = p.arms + ((size_t)inst * K + a_upd) * R::R;
+        for (int c = tid; c < R::R; c += nthr) {
+            const int sl = c / G, jj = c % G;
+            float v[4];
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                const int ci = canon(D, jj, 4 * sl + qq);
+                v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
+            }
+            dst[c] = make_float4(v[0], v[1], v[2], v[3]);
+        }
         if (tid == 0) p.nsel[(size_t)inst * K + a_upd] += 1;
         if (x_ok && wave == 0) {
             // score the updated arm on x_t from LDS, in the streaming order
-            float vj = 0.0f;
+            float f[4 * S];
 #pragma unroll
-            for (int i = 0; i < D; ++i)
-                if (i <= lane) vj = fmaf(sn[D + packed(i, lane < D ? lane : 0)], x[i], vj);
-            float ma = 0.0f, w2a = 0.0f;
-#pragma unroll
-            for (int j = 0; j < D; ++j) {
-                const float v = __shfl(vj, j);
-                w2a = fmaf(v, v, w2a);
-                ma = fmaf(sn[j], x[j], ma);
+            for (int e = 0; e < 4 * S; ++e) {
+                const int ci = canon(D, j, e);
+                f[e] = ci >= 0 ? s_new[ci] : 0.0f;
             }
+            float m, w2;
+            slice_terms<D>(f, xa, xb, xt0, xt1, m, w2);
+            m = group_sum<G>(m);
+            w2 = group_sum<G>(w2);
             if (lane == 0) {
-                s_scal[2] = ma;
-                s_scal[3] = w2a;
+                const float w = sqrtf(w2);
+                s_ucb[a_upd] = fmaf(p.alpha, w, m);
+                s_lcb[a_upd] = fmaf(-p.alpha, w, m);
             }
-        }
-        __syncthreads();
-        if (x_ok && k == a_upd) {
-            m = s_scal[2];
-            w2 = s_scal[3];
         }
     } else if (has_prev && tid == 0) {
         blk[kInstBad] += 1;
@@ -384,57 +480,64 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
         }
         return;
     }
+    __syncthreads();
 
-    float ucb = -INFINITY, lcb = -INFINITY;
-    if (active) {
-        const float w = sqrtf(fmaxf(w2, 0.0f));
-        ucb = fmaf(p.alpha, w, m);
-        lcb = fmaf(-p.alpha, w, m);
-    }
-    if (p.scores != nullptr && k < K) {
-        float *sc = p.scores + (size_t)inst * 2 * K;
-        sc[k] = ucb;
-        sc[K + k] = lcb;
-    }
-
-    // ---- pruning and argmax ----
-    bool keep = active;
+    // ---- pruning and argmax over the scores in LDS ----
+    auto is_active = [&](int k) { return k < K && ((s_mask[k >> 5] >> (k & 31)) & 1u) != 0; };
+    float lstar = -INFINITY;
     if (p.prune_now) {
-        float l = active ? lcb : -INFINITY;
+        float l = -INFINITY;
+        for (int k = tid; k < K; k += nthr)
+            if (is_active(k)) l = fmaxf(l, s_lcb[k]);
         for (int off = kWave / 2; off > 0; off >>= 1) l = fmaxf(l, __shfl_xor(l, off));
         if (lane == 0) s_red_v[wave] = l;
         __syncthreads();
-        float lstar = -INFINITY;
         for (int w = 0; w < nwave; ++w) lstar = fmaxf(lstar, s_red_v[w]);
-        keep = active && !(ucb < lstar);
         __syncthreads();
     }
-    const unsigned long long bal = __ballot(keep);
-    if (p.prune_now) {
-        uint32_t *mwo = p.mask + (size_t)inst * p.KW;
-        const int w0 = 2 * wave;
-        if (lane == 0 && w0 < p.KW) mwo[w0] = (uint32_t)(bal & 0xffffffffull);
-        if (lane == 0 && w0 + 1 < p.KW) mwo[w0 + 1] = (uint32_t)(bal >> 32);
+    BestPair b{-INFINITY, 0x7fffffff};
+    int n = 0;
+    float *sc = p.scores != nullptr ? p.scores + (size_t)inst * 2 * K : nullptr;
+    for (int base = 0; base < K; base += nthr) {
+        const int k = base + tid;
+        const bool act = is_active(k);
+        const float u = act ? s_ucb[k] : -INFINITY;
+        const bool keep = act && !(u < lstar);
+        if (keep) {
+            b = better(b, BestPair{u, k});
+            ++n;
+        }
+        if (sc != nullptr && k < K) {
+            sc[k] = u;
+            sc[K + k] = act ? s_lcb[k] : -INFINITY;
+        }
+        if (p.prune_now) {
+            const unsigned long long bal = __ballot(keep);
+            const int w0 = (base + wave * kWave) >> 5;
+            uint32_t *mwo = p.mask + (size_t)inst * KW;
+            if (lane == 0 && w0 < KW) mwo[w0] = (uint32_t)(bal & 0xffffffffull);
+            if (lane == 0 && w0 + 1 < KW) mwo[w0 + 1] = (uint32_t)(bal >> 32);
+        }
     }
-    BestPair b{keep ? ucb : -INFINITY, keep ? k : 0x7fffffff};
     for (int off = kWave / 2; off > 0; off >>= 1) {
         BestPair o{__shfl_xor(b.v, off), __shfl_xor(b.k, off)};
         b = better(b, o);
+        n += __shfl_xor(n, off);
     }
     if (lane == 0) {
         s_red_v[wave] = b.v;
         s_red_k[wave] = b.k;
-        s_red_n[wave] = __popcll(bal);
+        s_red_n[wave] = n;
     }
     __syncthreads();
     if (wave == 0) {
         // every lane of wavefront 0 reduces the per-wave results, then the
         // lanes write the instance block (action, count, context) at once
         BestPair best{s_red_v[0], s_red_k[0]};
-        int n = s_red_n[0];
+        int cnt = s_red_n[0];
         for (int w = 1; w < nwave; ++w) {
             best = better(best, BestPair{s_red_v[w], s_red_k[w]});
-            n += s_red_n[w];
+            cnt += s_red_n[w];
         }
         const int a = best.k == 0x7fffffff ? -1 : best.k;
         if (lane == 0) {
@@ -445,9 +548,9 @@ __global__ __launch_bounds__(1024) void agft_step_kernel(StepArgs p) {
             }
         }
         if (lane == kInstAprev) blk[kInstAprev] = a;
-        if (lane == kInstKact) blk[kInstKact] = n;
+        if (lane == kInstKact) blk[kInstKact] = cnt;
         if (lane >= kInstX && lane < kInstX + D)
-            reinterpret_cast<float *>(blk)[lane] = x_lane<D>(x, lane - kInstX);
+            reinterpret_cast<float *>(blk)[lane] = pick<D>(x, lane - kInstX);
     }
 }
 
@@ -467,16 +570,19 @@ struct InitArgs {
 __global__ void agft_init_kernel(InitArgs p) {
     const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t gsz = (size_t)gridDim.x * blockDim.x;
-    const size_t nrec = (size_t)p.B * p.C * p.K;
-    const int nt = p.d / 4;
+    const size_t nrec = (size_t)p.B * p.K * p.C;
+    const int G = p.d / 2;
     for (size_t idx = gtid; idx < nrec; idx += gsz) {
-        const int c = (int)((idx / p.K) % p.C);
-        float v[4] = {0.f, 0.f, 0.f, 0.f};
-        if (c >= nt) {
-            for (int q = 0; q < 4; ++q) {
-                int i, j;
-                unpack(4 * (c - nt) + q, i, j);
-                v[q] = (i == j) ? p.inv_sqrt_lambda : 0.0f;
+        const int c = (int)(idx % p.C);
+        const int sl = c / G, jj = c % G;
+        float v[4];
+        for (int q = 0; q < 4; ++q) {
+            const int ci = canon(p.d, jj, 4 * sl + q);
+            v[q] = 0.0f;
+            if (ci >= p.d) {
+                int i, col;
+                unpack(ci - p.d, i, col);
+                if (i == col) v[q] = p.inv_sqrt_lambda;
             }
         }
         p.arms[idx] = make_float4(v[0], v[1], v[2], v[3]);
@@ -500,24 +606,24 @@ __global__ void agft_export_kernel(const float4 *arms, int B, int K, float *thet
     using R = Rec<D>;
     const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid >= (size_t)B * K) return;
-    const size_t inst = gid / K;
-    const int k = (int)(gid % K);
-    float rec[R::F];
-    for (int c = 0; c < R::C; ++c) {
-        const float4 v = arms[(inst * R::C + c) * K + k];
-        rec[4 * c + 0] = v.x;
-        rec[4 * c + 1] = v.y;
-        rec[4 * c + 2] = v.z;
-        rec[4 * c + 3] = v.w;
+    float can[R::CAN];
+    for (int c = 0; c < R::R; ++c) {
+        const float4 v = arms[gid * R::R + c];
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+        const int sl = c / R::G, jj = c % R::G;
+        for (int q = 0; q < 4; ++q) {
+            const int ci = canon(D, jj, 4 * sl + q);
+            if (ci >= 0) can[ci] = vv[q];
+        }
     }
     if (theta != nullptr)
-        for (int i = 0; i < D; ++i) theta[gid * D + i] = rec[i];
+        for (int i = 0; i < D; ++i) theta[gid * D + i] = can[i];
     if (ainv != nullptr) {
-        const float *S = rec + D;
+        const float *S = can + D;
         for (int r = 0; r < D; ++r)
             for (int c = 0; c < D; ++c) {
                 float acc = 0.0f;
-                for (int j = (r > c ? r : c); j < D; ++j) acc = fmaf(S[packed(r, j)], S[packed(c, j)], acc);
+                for (int jc = (r > c ? r : c); jc < D; ++jc) acc = fmaf(S[packed(r, jc)], S[packed(c, jc)], acc);
                 ainv[(gid * D + r) * D + c] = acc;
             }
     }
@@ -675,8 +781,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.prune_now = (d_ctx != nullptr && c.prune_rule == 1 && t > 0 && t % c.prune_period == 0) ? 1 : 0;
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
-    const int threads = ((c.K + kWave - 1) / kWave) * kWave;
-    const dim3 grid((unsigned)c.B), block((unsigned)threads);
+    const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves_for(c.K, c.d)));
     switch (c.d) {
         case 8: hipLaunchKernelGGL(agft_step_kernel<8>, grid, block, 0, h->stream, p); break;
         case 16: hipLaunchKernelGGL(agft_step_kernel<16>, grid, block, 0, h->stream, p); break;

@@ -106,7 +106,7 @@ class Tuner:
         inst = region(v.inst, B * IW, torch.int32, (B, IW))
         return dict(
             t=int(v.t), pending=int(v.pending),
-            arms=region(v.arms, B * C * K * 4, torch.float32, (B, C, K, 4)),
+            arms=region(v.arms, B * K * C * 4, torch.float32, (B, K, C, 4)),
             mask=region(v.mask, B * KW, torch.int32, (B, KW)),
             inst=inst,
             aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2],

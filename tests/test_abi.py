@@ -50,10 +50,12 @@ def _cfg(**kw):
 def test_state_bytes(lib):
     n = L.agft_state_bytes(_cfg())
     assert n > 0 and n % 256 == 0
-    # arms region: B * (d/4 + d(d+1)/8) chunks * K * 16 bytes dominates
-    big = L.agft_state_bytes(_cfg(B=65536, K=128, d=16))
-    assert big >= 65536 * 38 * 128 * 16
-    assert big < 65536 * 38 * 128 * 16 * 1.02
+    # the arm records dominate: B * K * (d/2) * ((d+6)/4) float4 chunks
+    # (d + d(d+1)/2 floats per arm, padded to whole chunks per lane slice)
+    for d, chunks in ((8, 12), (16, 40), (32, 144)):
+        assert 4 * chunks >= d + d * (d + 1) // 2
+        big = L.agft_state_bytes(_cfg(B=4096, K=128, d=d))
+        assert 4096 * 128 * chunks * 16 <= big < 4096 * 128 * chunks * 16 * 1.05
     for bad in (dict(B=0), dict(K=0), dict(K=1025), dict(lambda_=0.0), dict(lambda_=float("nan")),
                 dict(alpha0=-1.0), dict(alpha0=float("inf")), dict(alpha_sched=2),
                 dict(prune_rule=3), dict(prune_period=0), dict(flags=4), dict(d=12)):
