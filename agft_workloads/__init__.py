@@ -6,8 +6,10 @@ arithmetic (no LinUCB scoring or update, no energy-delay model): it only
 defines sizes, constants and random draws that both the GPU path and the
 CPU oracle consume as inputs.
 """
-from .configs import WORKLOADS, ENV, Workload, get_workload, arm_values
+from .configs import (WORKLOADS, ENV, Workload, get_workload, arm_values, with_paper_pruning,
+                      PAPER_PRUNING)
 from .traces import exogenous, probe_instances
 
-__all__ = ["WORKLOADS", "ENV", "Workload", "get_workload", "arm_values",
+__all__ = ["WORKLOADS", "ENV", "Workload", "get_workload", "arm_values", "with_paper_pruning",
+           "PAPER_PRUNING",
            "exogenous", "probe_instances"]

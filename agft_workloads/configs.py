@@ -26,16 +26,39 @@ class Workload:
     lam: float           # ridge prior: A_k(0) = lam * I
     alpha0: float        # exploration weight
     alpha_sched: int     # 0: alpha_t = alpha0; 1: alpha_t = alpha0 / sqrt(t + 1)
-    prune: int           # 0: off; 1: drop arm k when UCB_k < max_j LCB_j
+    prune: int           # rule mask: 1 drop arm k when UCB_k < max_j LCB_j (every
+                         # `period` steps); 2 extreme-frequency, 4 historical-
+                         # performance, 8 cascade pruning (Sec. 4.3)
     period: int          # prune evaluated at t > 0 with t % period == 0
     trace: str           # load-trace family, see traces.py
     drift: float = 0.0   # power/latency coefficients b, c scale to (1 + drift) at t = T - 1
     description: str = ""
+    # the paper's pruning heuristics (rule bits 2, 4, 8; Sec. 4.3): the example
+    # values the paper gives, plus this build's reading of the unstated ones
+    # (tolerance multiplier and the minimum number of compared arms)
+    ext_rounds: int = 60
+    ext_min_n: int = 3
+    ext_thr: float = -1.2
+    hist_after: int = 30
+    hist_min_n: int = 6
+    hist_kappa: float = 1.0
+    hist_min_arms: int = 3
 
     @property
     def arm_record_floats(self) -> int:
         """Floats of per-arm bandit state the GPU path keeps (theta + packed factor)."""
         return self.d + self.d * (self.d + 1) // 2
+
+    @property
+    def cascade_k(self) -> int:
+        """Arms whose clock is below half of the top clock (cascade rule)."""
+        return sum(1 for f in arm_values(self.K) if f < 0.5 * ENV["f_hi"])
+
+    def heuristics(self) -> dict:
+        return dict(ext_rounds=self.ext_rounds, ext_min_n=self.ext_min_n, ext_thr=self.ext_thr,
+                    hist_after=self.hist_after, hist_min_n=self.hist_min_n,
+                    hist_kappa=self.hist_kappa, hist_min_arms=self.hist_min_arms,
+                    cascade_k=self.cascade_k)
 
     def alpha_at(self, t: int) -> float:
         if self.alpha_sched == 0:
@@ -64,12 +87,28 @@ WORKLOADS = {
 }
 
 
+PAPER_PRUNING = 2 | 4 | 8
+
+
+def with_paper_pruning(wl: Workload) -> Workload:
+    """The same workload with the paper's pruning heuristics added to its rules."""
+    d = dict(wl.__dict__)
+    d["prune"] = wl.prune | PAPER_PRUNING
+    d["name"] = wl.name + "p"
+    d["description"] = wl.description + ", plus the paper's extreme/historical/cascade pruning"
+    return Workload(**d)
+
+
 def get_workload(cfg, **overrides) -> Workload:
     """Workload by id (1..5) or name ("cfg4"), optionally with fields replaced
     (smaller B or T for quick parity cases)."""
+    paper = False
     if isinstance(cfg, str):
-        cfg = int(cfg.replace("cfg", ""))
+        paper = cfg.endswith("p")
+        cfg = int(cfg.replace("cfg", "").rstrip("p"))
     wl = WORKLOADS[cfg]
+    if paper:
+        wl = with_paper_pruning(wl)
     if overrides:
         d = dict(wl.__dict__)
         d.update(overrides)

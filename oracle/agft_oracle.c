@@ -20,11 +20,24 @@
  * alpha_t is alpha0 or alpha0 / sqrt(t + 1); ties go to the lowest arm index;
  * a negative rounding of the quadratic form is taken as 0 under the root.
  *
- * Pruning (the confidence-bound rule of the workloads; motivation in Sec. 4.3,
- * where pruned arms leave the action space for good): at a step t > 0 with
- * t % period == 0, an active arm k stays active iff UCB_k >= max over the
- * active arms j of LCB_j, all scores taken with that step's x_t and alpha_t,
- * before that step's argmax.
+ * Pruning; every rule removes arms for good ("permanently removed", Sec. 4.3).
+ * The rule set is a bit mask:
+ *   1  confidence bounds: at a step t > 0 with t % period == 0, an active arm
+ *      k stays active iff UCB_k >= max over the active arms j of LCB_j, all
+ *      scores taken with that step's x_t and alpha_t, before the argmax;
+ *   2  extreme-frequency pruning (Sec. 4.3): while t < ext_rounds, an active
+ *      arm with n_k >= ext_min_n rewards and mean reward below ext_thr goes;
+ *   4  historical-performance pruning (Sec. 4.3): once t >= hist_after, among
+ *      the active arms with n_k >= hist_min_n (at least hist_min_arms of
+ *      them) an arm goes when the best of their mean rewards exceeds its own
+ *      by more than hist_kappa times the (population) standard deviation of
+ *      those means;
+ *   8  cascade pruning (Sec. 4.3): when rule 2 or 4 removes an arm below
+ *      half of the top clock (index < cascade_k), every lower arm goes too.
+ * Rules 2-8 act on the arms active at the start of the step, after the
+ * previous decision's reward has been folded in and before scoring; rules 2
+ * and 4 are judged together.  If they would leave no arm, the one with the
+ * best mean reward (lowest index on ties) stays.
  *
  * The paper gives the update as Eq. 3-5: A and b are accumulated as written
  * and A_k^{-1} is recomputed by Gauss-Jordan elimination with partial
@@ -54,12 +67,16 @@
 typedef struct {
     int B, K, d, prune, period, sched;
     double lambda, alpha0;
+    /* parameters of rules 2-8 */
+    int ext_rounds, ext_min_n, hist_after, hist_min_n, hist_min_arms, cascade_k;
+    double ext_thr, hist_kappa;
     double *A;              /* [B][K][d][d]  Eq. 3 */
     double *b;              /* [B][K][d]     Eq. 4 */
     double *Ainv;           /* [B][K][d][d]  inverse of A */
     double *theta;          /* [B][K][d]     Eq. 5 */
     unsigned char *active;  /* [B][K]        current action set */
-    int *nsel;              /* [B][K]        times each arm was updated */
+    int *nsel;              /* [B][K]        rewards folded into each arm */
+    double *rsum;           /* [B][K]        sum of those rewards */
     double *xprev;          /* [B][d]        context of the last decision */
     int *aprev;             /* [B]           last decision (-1: none) */
     int *bad;               /* [B]           non-finite inputs seen */
@@ -100,6 +117,10 @@ static int gauss_jordan_inverse(int d, const double *M, double *out)
     return 0;
 }
 
+void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, double *lcb,
+                   unsigned char *keep, int *action, double *margins);
+void ora_get_rsum(const void *h, int i, double *rsum);
+
 static int all_finite(const double *v, int n)
 {
     for (int i = 0; i < n; ++i)
@@ -110,7 +131,7 @@ static int all_finite(const double *v, int n)
 void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
                  int prune, int period)
 {
-    if (B < 1 || K < 1 || d < 1 || d > ORA_MAXD || !(lambda > 0.0) || period < 1)
+    if (B < 1 || K < 1 || K > 1024 || d < 1 || d > ORA_MAXD || !(lambda > 0.0) || period < 1)
         return NULL;
     ora_t *o = (ora_t *)calloc(1, sizeof(ora_t));
     if (!o) return NULL;
@@ -123,13 +144,14 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
     o->theta = (double *)calloc(nk * d, sizeof(double));
     o->active = (unsigned char *)malloc(nk);
     o->nsel = (int *)calloc(nk, sizeof(int));
+    o->rsum = (double *)calloc(nk, sizeof(double));
     o->xprev = (double *)calloc((size_t)B * d, sizeof(double));
     o->aprev = (int *)malloc((size_t)B * sizeof(int));
     o->bad = (int *)calloc((size_t)B, sizeof(int));
-    if (!o->A || !o->b || !o->Ainv || !o->theta || !o->active || !o->nsel ||
+    if (!o->A || !o->b || !o->Ainv || !o->theta || !o->active || !o->nsel || !o->rsum ||
         !o->xprev || !o->aprev || !o->bad) {
         free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
-        free(o->nsel); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+        free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad); free(o);
         return NULL;
     }
     /* A_k(0) = lambda I, b_k(0) = 0, hence A_k^{-1}(0) = I / lambda, theta_k(0) = 0. */
@@ -148,7 +170,17 @@ void ora_destroy(void *h)
     ora_t *o = (ora_t *)h;
     if (!o) return;
     free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
-    free(o->nsel); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+    free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+}
+
+/* Parameters of pruning rules 2-8 (see the header). */
+void ora_set_heuristics(void *h, int ext_rounds, int ext_min_n, double ext_thr, int hist_after,
+                        int hist_min_n, double hist_kappa, int hist_min_arms, int cascade_k)
+{
+    ora_t *o = (ora_t *)h;
+    o->ext_rounds = ext_rounds; o->ext_min_n = ext_min_n; o->ext_thr = ext_thr;
+    o->hist_after = hist_after; o->hist_min_n = hist_min_n; o->hist_kappa = hist_kappa;
+    o->hist_min_arms = hist_min_arms; o->cascade_k = cascade_k;
 }
 
 /* Eq. 3-5 for arm k of instance i with context x and reward r. */
@@ -168,6 +200,72 @@ static void update_arm(ora_t *o, int i, int k, const double *x, double r)
         theta[p] = s;
     }
     o->nsel[ik] += 1;
+    o->rsum[ik] += r;
+}
+
+/* Rules 2-8 for instance i at step t: act1 = arms that stay, from act0.
+ * margin[k] = distance of arm k's closest rule-2/4 comparison from its
+ * threshold (INFINITY when no such rule applied to it). */
+static void heuristic_prune(const ora_t *o, int i, long t, const unsigned char *act0,
+                            unsigned char *act1, double *margin)
+{
+    const int K = o->K;
+    const int *n = o->nsel + (size_t)i * K;
+    const double *rs = o->rsum + (size_t)i * K;
+    unsigned char gone[1024];
+    double mean[1024];
+    for (int k = 0; k < K; ++k) {
+        mean[k] = n[k] > 0 ? rs[k] / n[k] : 0.0;
+        gone[k] = 0;
+        margin[k] = INFINITY;
+    }
+    if ((o->prune & 2) && t < o->ext_rounds)
+        for (int k = 0; k < K; ++k)
+            if (act0[k] && n[k] >= o->ext_min_n) {
+                double m = mean[k] - o->ext_thr;
+                if (fabs(m) < margin[k]) margin[k] = fabs(m);
+                if (m < 0.0) gone[k] = 1;
+            }
+    if ((o->prune & 4) && t >= o->hist_after) {
+        int q = 0;
+        double best = -INFINITY, sum = 0.0;
+        for (int k = 0; k < K; ++k)
+            if (act0[k] && n[k] >= o->hist_min_n) {
+                ++q;
+                sum += mean[k];
+                if (mean[k] > best) best = mean[k];
+            }
+        if (q >= o->hist_min_arms && q > 0) {
+            double mu = sum / q, var = 0.0;
+            for (int k = 0; k < K; ++k)
+                if (act0[k] && n[k] >= o->hist_min_n) var += (mean[k] - mu) * (mean[k] - mu);
+            double sigma = sqrt(var / q);
+            for (int k = 0; k < K; ++k)
+                if (act0[k] && n[k] >= o->hist_min_n) {
+                    double m = o->hist_kappa * sigma - (best - mean[k]);
+                    if (fabs(m) < margin[k]) margin[k] = fabs(m);
+                    if (m < 0.0) gone[k] = 1;
+                }
+        }
+    }
+    if (o->prune & 8) {
+        int kstar = -1;
+        for (int k = 0; k < K; ++k)
+            if (gone[k] && k < o->cascade_k) kstar = k;
+        for (int k = 0; k < kstar; ++k) gone[k] = 1;
+    }
+    int left = 0;
+    for (int k = 0; k < K; ++k) {
+        act1[k] = act0[k] && !gone[k];
+        left += act1[k];
+    }
+    if (left == 0) {
+        int keep = -1;
+        for (int k = 0; k < K; ++k)
+            if (act0[k] && (keep < 0 || (n[k] > 0 && (n[keep] == 0 || mean[k] > mean[keep]))))
+                keep = k;
+        if (keep >= 0) act1[keep] = 1;
+    }
 }
 
 static void apply_pending(ora_t *o, int i, const double *r)
@@ -197,21 +295,41 @@ double ora_alpha(const void *h, long t)
 void ora_decide(void *h, const double *x, const double *r, double *ucb, double *lcb,
                 unsigned char *keep, int *action)
 {
+    ora_decide_ex(h, x, r, ucb, lcb, keep, action, NULL);
+}
+
+/* ora_decide, also returning the rule-2/4 margins [B][K] (may be NULL). */
+void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, double *lcb,
+                   unsigned char *keep, int *action, double *margins)
+{
     ora_t *o = (ora_t *)h;
     const int B = o->B, K = o->K, d = o->d;
     const long t = o->t;
     const int pending = o->pending;
     const double alpha = ora_alpha(o, t);
-    const int prune_now = o->prune && t > 0 && (t % o->period) == 0;
+    const int prune_now = (o->prune & 1) && t > 0 && (t % o->period) == 0;
 #pragma omp parallel for schedule(dynamic, 4)
     for (int i = 0; i < B; ++i) {
         if (pending) apply_pending(o, i, r);
         const double *xi = x + (size_t)i * d;
+        unsigned char act1[1024];
+        double marg[1024];
         const unsigned char *act = o->active + (size_t)i * K;
         double *U = ucb + (size_t)i * K, *L = lcb + (size_t)i * K;
         unsigned char *kp = keep + (size_t)i * K;
-        for (int k = 0; k < K; ++k) { U[k] = -INFINITY; L[k] = -INFINITY; kp[k] = act[k]; }
-        if (!all_finite(xi, d)) { o->bad[i] += 1; action[i] = -1; continue; }
+        for (int k = 0; k < K; ++k) { U[k] = -INFINITY; L[k] = -INFINITY; kp[k] = act[k]; marg[k] = INFINITY; }
+        if (!all_finite(xi, d)) {
+            o->bad[i] += 1;
+            action[i] = -1;
+            if (margins) memcpy(margins + (size_t)i * K, marg, sizeof(double) * K);
+            continue;
+        }
+        if (o->prune & 14) {
+            heuristic_prune(o, i, t, act, act1, marg);
+            act = act1;
+            for (int k = 0; k < K; ++k) kp[k] = act[k];
+        }
+        if (margins) memcpy(margins + (size_t)i * K, marg, sizeof(double) * K);
         for (int k = 0; k < K; ++k) {
             if (!act[k]) continue;
             size_t ik = (size_t)i * K + k;
@@ -270,6 +388,7 @@ void ora_flush(void *h, const double *r)
 void ora_get(const void *h, int i, double *A, double *b, double *Ainv, double *theta,
              unsigned char *active, int *nsel, int *bad)
 {
+    ora_get_rsum(h, i, NULL);
     const ora_t *o = (const ora_t *)h;
     const int K = o->K, d = o->d;
     size_t base = (size_t)i * K;
@@ -280,6 +399,13 @@ void ora_get(const void *h, int i, double *A, double *b, double *Ainv, double *t
     if (active) memcpy(active, o->active + base, K);
     if (nsel) memcpy(nsel, o->nsel + base, sizeof(int) * K);
     if (bad) *bad = o->bad[i];
+}
+
+/* Sum of the rewards folded into each arm of instance i ([K]). */
+void ora_get_rsum(const void *h, int i, double *rsum)
+{
+    const ora_t *o = (const ora_t *)h;
+    if (rsum) memcpy(rsum, o->rsum + (size_t)i * o->K, sizeof(double) * o->K);
 }
 
 long ora_t_now(const void *h) { return ((const ora_t *)h)->t; }

@@ -30,6 +30,9 @@ def _declare(lib):
     lib.ora_create.argtypes = [I, I, I, D, D, I, I, I]
     lib.ora_destroy.argtypes = [P]
     lib.ora_decide.argtypes = [P, P, P, P, P, P, P]
+    lib.ora_decide_ex.argtypes = [P, P, P, P, P, P, P, P]
+    lib.ora_set_heuristics.argtypes = [P, I, I, D, I, I, D, I, I]
+    lib.ora_get_rsum.argtypes = [P, I, P]
     lib.ora_commit.argtypes = [P, P, P, P]
     lib.ora_flush.argtypes = [P, P]
     lib.ora_get.argtypes = [P, I, P, P, P, P, P, P, P]
@@ -72,8 +75,18 @@ class Oracle:
 
     @classmethod
     def from_workload(cls, wl, B=None, lib=None):
-        return cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0,
-                   wl.alpha_sched, wl.prune, wl.period, lib=lib)
+        o = cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0,
+                wl.alpha_sched, wl.prune, wl.period, lib=lib)
+        if wl.prune & 14:
+            o.set_heuristics(**wl.heuristics())
+        return o
+
+    def set_heuristics(self, ext_rounds, ext_min_n, ext_thr, hist_after, hist_min_n, hist_kappa,
+                       hist_min_arms, cascade_k):
+        """Parameters of the paper's pruning rules (bits 2, 4, 8 of the rule mask)."""
+        self.lib.ora_set_heuristics(self.h, int(ext_rounds), int(ext_min_n), float(ext_thr),
+                                    int(hist_after), int(hist_min_n), float(hist_kappa),
+                                    int(hist_min_arms), int(cascade_k))
 
     def __del__(self):
         h = getattr(self, "h", None)
@@ -88,18 +101,23 @@ class Oracle:
     def alpha(self, t=None):
         return float(self.lib.ora_alpha(self.h, self.t if t is None else int(t)))
 
-    def decide(self, x, r=None):
+    def decide(self, x, r=None, margins=False):
         """Apply the pending update, score x_t, prune, pick a_t.
 
-        Returns (ucb [B][K], lcb [B][K], keep [B][K] bool, action [B])."""
+        Returns (ucb [B][K], lcb [B][K], keep [B][K] bool, action [B]) and, with
+        margins=True, also the per-arm distances of the rule-2/4 comparisons
+        from their thresholds [B][K] (inf where no such rule applied)."""
         x = np.ascontiguousarray(x, dtype=np.float64).reshape(self.B, self.d)
         r = None if r is None else np.ascontiguousarray(r, dtype=np.float64).reshape(self.B)
         ucb = np.empty((self.B, self.K))
         lcb = np.empty((self.B, self.K))
         keep = np.empty((self.B, self.K), dtype=np.uint8)
         action = np.empty(self.B, dtype=np.int32)
-        self.lib.ora_decide(self.h, _ptr(x), _ptr(r), _ptr(ucb), _ptr(lcb), _ptr(keep),
-                            _ptr(action))
+        marg = np.empty((self.B, self.K)) if margins else None
+        self.lib.ora_decide_ex(self.h, _ptr(x), _ptr(r), _ptr(ucb), _ptr(lcb), _ptr(keep),
+                               _ptr(action), _ptr(marg))
+        if margins:
+            return ucb, lcb, keep.astype(bool), action, marg
         return ucb, lcb, keep.astype(bool), action
 
     def commit(self, x, action, keep):
@@ -129,6 +147,8 @@ class Oracle:
                          ctypes.byref(bad))
         out["active"] = out["active"].astype(bool)
         out["bad"] = bad.value
+        out["rsum"] = np.empty(K)
+        self.lib.ora_get_rsum(self.h, int(i), _ptr(out["rsum"]))
         return out
 
     @staticmethod

@@ -300,3 +300,143 @@ def pin_convergence_linear_reward(lib):
 ALL_PINS = [pin_brute_force_small, pin_repeated_update_closed_form, pin_ridge_least_squares,
             pin_rational_worked_example, pin_textbook_reductions, pin_prune_invariants,
             pin_convergence_linear_reward]
+
+
+# ---- the paper's pruning heuristics (rule bits 2, 4, 8; Sec. 4.3) ----
+
+def _scripted(lib, K, d, rule, heur, plan, x=None, lam=1.0, alpha=1.0):
+    """Drive one oracle instance with scripted actions and rewards.
+
+    plan: list of (action, reward); the action is committed whatever the
+    oracle proposes, so each arm's reward history is exactly the script.
+    Returns the decide() outputs of every step and the oracle."""
+    ora = Oracle(1, K, d, lam, alpha, 0, rule, 1000, lib=lib)
+    ora.set_heuristics(**heur)
+    x = np.ones((1, d)) if x is None else x
+    r_prev = None
+    outs = []
+    for a, r in plan:
+        ucb, lcb, keep, action, marg = ora.decide(x, r_prev, margins=True)
+        outs.append((ucb[0], keep[0], marg[0]))
+        ora.commit(x, np.array([a]), keep)
+        r_prev = np.array([r])
+    ucb, lcb, keep, action, marg = ora.decide(x, r_prev, margins=True)
+    outs.append((ucb[0], keep[0], marg[0]))
+    return outs, ora
+
+
+HEUR = dict(ext_rounds=60, ext_min_n=3, ext_thr=-1.2, hist_after=30, hist_min_n=6, hist_kappa=1.0,
+            hist_min_arms=3, cascade_k=0)
+
+
+def pin_extreme_pruning(lib):
+    """Sec. 4.3 extreme pruning: within the first 60 rounds an arm with at
+    least 3 rewards averaging below -1.2 leaves for good; 2 rewards are not
+    enough, a mean at -1.1 stays, and after round 60 the rule is off."""
+    plan = [(1, -1.5), (1, -1.4), (1, -1.6),      # arm 1: n = 3, mean -1.5
+            (2, -1.1), (2, -1.1), (2, -1.1),      # arm 2: n = 3, mean -1.1
+            (3, -5.0), (3, -5.0)]                 # arm 3: n = 2
+    outs, ora = _scripted(lib, 5, 2, 2, HEUR, plan)
+    ucb, keep, marg = outs[-1]
+    assert list(keep) == [True, False, True, True, True]
+    assert ucb[1] == -np.inf and np.isfinite(ucb[3])
+    assert marg[1] == np.inf and abs(marg[2] - 0.1) < 1e-12 and marg[3] == np.inf
+    assert abs(outs[3][2][1] - 0.3) < 1e-12      # judged at step 3, gone afterwards
+    # arm 1 leaves at the decision after its third reward (step 3), not before
+    assert outs[2][1][1] and not outs[3][1][1]
+    # the third reward lands at round 59 (judged) or round 60 (too late)
+    outs, _ = _scripted(lib, 5, 2, 2, HEUR, [(0, -1.0)] * 56 + [(4, -2.0)] * 3)
+    assert not outs[-1][1][4]
+    outs, _ = _scripted(lib, 5, 2, 2, HEUR, [(0, -1.0)] * 57 + [(4, -2.0)] * 3)
+    assert outs[-1][1][4]
+
+
+def pin_historical_pruning(lib):
+    """Sec. 4.3 historical pruning, worked by hand: qualifying arms' mean
+    rewards -1, -1.1, -2, -1.05 have mean -1.2875 and population standard
+    deviation 0.41288; only the arm 1.0 below the best is more than one
+    deviation worse.  With too few qualifying arms nothing is compared."""
+    heur = dict(HEUR, hist_after=0, hist_min_n=1, hist_min_arms=4)
+    plan = [(0, -1.0), (1, -1.1), (2, -2.0), (3, -1.05)]
+    outs, _ = _scripted(lib, 5, 2, 4, heur, plan)
+    ucb, keep, marg = outs[-1]
+    assert list(keep) == [True, True, False, True, True]
+    sigma = 0.41288
+    assert abs(marg[2] - (1.0 - sigma)) < 1e-5 and abs(marg[0] - sigma) < 1e-5
+    outs, _ = _scripted(lib, 5, 2, 4, heur, plan[:2])
+    assert outs[-1][1].all()
+    # hist_after: the rule waits for its round
+    outs, _ = _scripted(lib, 5, 2, 4, dict(heur, hist_after=10), plan)
+    assert outs[-1][1].all()
+
+
+def pin_cascade_pruning(lib):
+    """Sec. 4.3 cascade: an arm pruned below half of the top clock (index <
+    cascade_k) takes every lower arm with it; one above does not."""
+    heur = dict(HEUR, cascade_k=4)
+    plan = [(2, -2.0)] * 3 + [(1, -0.5)] * 3
+    outs, _ = _scripted(lib, 6, 2, 2 | 8, heur, plan)
+    assert list(outs[3][1]) == [False, False, False, True, True, True]
+    plan = [(4, -2.0)] * 3
+    outs, _ = _scripted(lib, 6, 2, 2 | 8, heur, plan)
+    assert list(outs[-1][1]) == [True, True, True, True, False, True]
+
+
+def pin_heuristics_keep_one_arm(lib):
+    """If the rules would remove every arm, the one with the best mean reward
+    stays: arm 2 fails the extreme rule and its cascade takes arms 0 and 1
+    (cascade_k = 3); arm 1's mean, -0.4, is the best."""
+    plan = [(0, -0.5), (1, -0.4)] + [(2, -2.0)] * 3
+    outs, _ = _scripted(lib, 3, 2, 2 | 8, dict(HEUR, cascade_k=3), plan)
+    assert list(outs[-1][1]) == [False, True, False]
+
+
+def pin_heuristics_brute_force(lib):
+    """Random scripted histories against an independent restatement of the
+    rules (numpy, vectorised), step by step."""
+    rng = np.random.default_rng(11)
+    for trial in range(6):
+        K = int(rng.integers(4, 12))
+        heur = dict(ext_rounds=int(rng.integers(5, 40)), ext_min_n=int(rng.integers(1, 4)),
+                    ext_thr=float(rng.uniform(-1.6, -0.9)), hist_after=int(rng.integers(0, 30)),
+                    hist_min_n=int(rng.integers(1, 5)), hist_kappa=float(rng.uniform(0.3, 2.0)),
+                    hist_min_arms=int(rng.integers(2, 5)), cascade_k=int(rng.integers(0, K)))
+        rule = int(rng.choice([2, 4, 8 | 2, 8 | 4, 14]))
+        ora = Oracle(1, K, 3, 1.0, 0.7, 0, rule, 1000, lib=lib)
+        ora.set_heuristics(**heur)
+        n = np.zeros(K, int)
+        s = np.zeros(K)
+        active = np.ones(K, bool)
+        x = np.array([[1.0, 0.3, -0.2]])
+        r_prev = None
+        for t in range(50):
+            ucb, lcb, keep, action = ora.decide(x, r_prev)
+            mean = np.where(n > 0, s / np.maximum(n, 1), 0.0)
+            gone = np.zeros(K, bool)
+            if rule & 2 and t < heur["ext_rounds"]:
+                gone |= active & (n >= heur["ext_min_n"]) & (mean < heur["ext_thr"])
+            q = active & (n >= heur["hist_min_n"])
+            if rule & 4 and t >= heur["hist_after"] and q.sum() >= heur["hist_min_arms"]:
+                sig = mean[q].std()
+                gone |= q & (mean[q].max() - mean > heur["hist_kappa"] * sig)
+            if rule & 8:
+                low = np.flatnonzero(gone & (np.arange(K) < heur["cascade_k"]))
+                if low.size:
+                    gone |= np.arange(K) < low.max()
+            stay = active & ~gone
+            if not stay.any():
+                cand = np.flatnonzero(active)
+                scored = [k for k in cand if n[k] > 0]
+                stay[max(scored, key=lambda k: (mean[k], -k)) if scored else cand[0]] = True
+            assert np.array_equal(keep[0], stay), (trial, t)
+            a = int(rng.choice(np.flatnonzero(stay)))
+            r = float(rng.normal(-1.2, 0.5))
+            ora.commit(x, np.array([a]), keep)
+            n[a] += 1
+            s[a] += r
+            active = stay
+            r_prev = np.array([r])
+
+
+ALL_PINS += [pin_extreme_pruning, pin_historical_pruning, pin_cascade_pruning,
+             pin_heuristics_keep_one_arm, pin_heuristics_brute_force]

@@ -31,6 +31,19 @@ MUTANTS = {
                                     "update_arm(o, i, a, o->xprev, r[i]);"),
     "width_without_root": ("double w = sqrt(quad > 0.0 ? quad : 0.0);",
                            "double w = quad > 0.0 ? quad : 0.0;"),
+    "extreme_threshold_sign": ("double m = mean[k] - o->ext_thr;", "double m = mean[k] + o->ext_thr;"),
+    "extreme_round_limit_inclusive": ("t < o->ext_rounds", "t <= o->ext_rounds"),
+    "extreme_min_samples_off_by_one": ("n[k] >= o->ext_min_n", "n[k] > o->ext_min_n"),
+    "historical_variance_not_rooted": ("double sigma = sqrt(var / q);", "double sigma = var / q;"),
+    "historical_min_arms_ignored": ("if (q >= o->hist_min_arms && q > 0)", "if (q > 0)"),
+    "historical_gap_reversed": ("double m = o->hist_kappa * sigma - (best - mean[k]);",
+                                "double m = o->hist_kappa * sigma - (mean[k] - best);"),
+    "cascade_prunes_upwards": ("for (int k = 0; k < kstar; ++k) gone[k] = 1;",
+                               "for (int k = kstar + 1; k < K; ++k) gone[k] = 1;"),
+    "cascade_threshold_inclusive": ("if (gone[k] && k < o->cascade_k) kstar = k;",
+                                    "if (gone[k] && k <= o->cascade_k) kstar = k;"),
+    "keep_one_worst_mean": ("(n[keep] == 0 || mean[k] > mean[keep])", "(n[keep] == 0 || mean[k] < mean[keep])"),
+    "reward_sum_not_kept": ("    o->rsum[ik] += r;", "    o->rsum[ik] += 0.0 * r;"),
 }
 
 
