@@ -60,12 +60,38 @@ typedef struct agft_config {
     float lambda;         /* ridge prior, A_k(0) = lambda I: finite, > 0 */
     float alpha0;         /* exploration weight of Eq. 1: finite, >= 0 */
     int32_t alpha_sched;  /* 0: alpha_t = alpha0; 1: alpha_t = alpha0 / sqrt(t + 1) */
-    int32_t prune_rule;   /* 0: none; 1: at a pruning step an active arm k is
-                             removed for good when UCB_k < max_j LCB_j over the
-                             active arms j, with that step's context and alpha_t,
-                             before the argmax */
-    int32_t prune_period; /* pruning steps are t > 0 with t % prune_period == 0; >= 1 */
+    int32_t prune_rule;   /* bit mask of pruning rules; every rule removes arms for good:
+                             1  confidence bounds: at steps t > 0 with
+                                t % prune_period == 0, an active arm k goes when
+                                UCB_k < max_j LCB_j over the active arms j, with that
+                                step's context and alpha_t, before the argmax;
+                             2  extreme-frequency pruning (Sec. 4.3): while
+                                t < ext_rounds, an active arm with at least
+                                ext_min_n rewards averaging below ext_thr goes;
+                             4  historical pruning (Sec. 4.3): once t >= hist_after,
+                                among the active arms with at least hist_min_n
+                                rewards (if there are hist_min_arms of them), an arm
+                                goes when the best of their mean rewards exceeds its
+                                own by more than hist_kappa times the population
+                                standard deviation of those means;
+                             8  cascade pruning (Sec. 4.3): when rule 2 or 4 removes
+                                an arm with index < cascade_k (clock below half of
+                                the top clock), every lower arm goes too.
+                             Rules 2-8 act on the arms active when the step starts,
+                             after the previous reward is folded in, before scoring;
+                             if they would leave no arm, the arm with the best mean
+                             reward (lowest index on ties) stays. */
+    int32_t prune_period; /* period of rule 1; >= 1 */
     uint32_t flags;       /* 0 or AGFT_ADOPT_STATE */
+    /* parameters of rules 2, 4, 8 (read only when the rule's bit is set) */
+    int32_t ext_rounds;    /* >= 0 */
+    int32_t ext_min_n;     /* >= 1 */
+    float ext_thr;         /* finite */
+    int32_t hist_after;    /* >= 0 */
+    int32_t hist_min_n;    /* >= 1 */
+    float hist_kappa;      /* finite, >= 0 */
+    int32_t hist_min_arms; /* >= 1 */
+    int32_t cascade_k;     /* 0..K */
 } agft_config;
 
 typedef struct agft_handle agft_handle;
@@ -92,11 +118,12 @@ typedef struct agft_state_view {
                            [2] non-finite contexts or rewards met, [3] reserved,
                            [4 .. 4+d) context of the last decision (fp32) */
     int32_t inst_words; /* words per instance block: 4 + d rounded up to 16 */
-    int32_t *nsel;      /* [B][K]: updates applied to each arm */
+    int32_t *stats;     /* [B][K][2] per arm: [0] rewards folded in (int32),
+                           [1] their sum (fp32 bits) */
 } agft_state_view;
 
 /* Bytes of device state for cfg (a 256-byte header, then the arm records,
- * the masks, the instance blocks and the update counts of agft_state_view,
+ * the masks, the instance blocks and the arm statistics of agft_state_view,
  * each region 256-byte aligned); 0 if cfg is invalid. */
 size_t agft_state_bytes(const agft_config *cfg);
 

@@ -8,12 +8,15 @@ from .env import Env
 from .oracle import Oracle
 
 
-def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, lib=None):
+def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, lib=None,
+                    margins=False):
     """Run T decisions of len(instances) tuners against the fp64 environment.
 
     arrivals, noise: [T+1][n] exogenous draws (agft_workloads.exogenous).
-    on_decide(t, x, r_prev, ucb, lcb, keep, action) may return (action, keep)
-    to commit instead of the oracle's own decision (a near-tied alternative).
+    on_decide(t, x, r_prev, ucb, lcb, keep, action[, margins]) may return
+    (action, keep) to commit instead of the oracle's own decision (a
+    near-tied alternative); with margins=True it also receives the distances
+    of the pruning-rule comparisons from their thresholds.
     Returns a dict with the oracle object, actions [T][n] and, if record is
     set, contexts [T][n][d], rewards [T][n] (reward of decision t) and
     ucb/lcb [T][n][K].
@@ -27,9 +30,13 @@ def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, l
     actions = np.empty((T, n), dtype=np.int32)
     rec = dict(x=[], r=[], ucb=[], lcb=[], keep=[]) if record else None
     for t in range(T):
-        ucb, lcb, keep, action = ora.decide(x, r_prev)
+        if margins:
+            ucb, lcb, keep, action, marg = ora.decide(x, r_prev, margins=True)
+        else:
+            ucb, lcb, keep, action = ora.decide(x, r_prev)
         if on_decide is not None:
-            over = on_decide(t, x, r_prev, ucb, lcb, keep, action)
+            args = (t, x, r_prev, ucb, lcb, keep, action) + ((marg,) if margins else ())
+            over = on_decide(*args)
             if over is not None:
                 action, keep = over
         ora.commit(x, action, keep)

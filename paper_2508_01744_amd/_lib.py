@@ -24,13 +24,16 @@ _i32, _u32, _f32, _i64, _sz, _vp = (ctypes.c_int32, ctypes.c_uint32, ctypes.c_fl
 class agft_config(ctypes.Structure):
     _fields_ = [("B", _i32), ("K", _i32), ("d", _i32), ("lambda_", _f32), ("alpha0", _f32),
                 ("alpha_sched", _i32), ("prune_rule", _i32), ("prune_period", _i32),
-                ("flags", _u32)]
+                ("flags", _u32),
+                ("ext_rounds", _i32), ("ext_min_n", _i32), ("ext_thr", _f32),
+                ("hist_after", _i32), ("hist_min_n", _i32), ("hist_kappa", _f32),
+                ("hist_min_arms", _i32), ("cascade_k", _i32)]
 
 
 class agft_state_view(ctypes.Structure):
     _fields_ = [("t", _i64), ("pending", _i32), ("B", _i32), ("K", _i32), ("d", _i32),
                 ("chunks", _i32), ("mask_words", _i32), ("arms", _vp), ("mask", _vp),
-                ("inst", _vp), ("inst_words", _i32), ("nsel", _vp)]
+                ("inst", _vp), ("inst_words", _i32), ("stats", _vp)]
 
 
 class agft_env_config(ctypes.Structure):

@@ -112,7 +112,7 @@ constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstX = 4;
 int inst_words(int d) { return (kInstX + d + 15) / 16 * 16; }
 
 struct Layout {
-    size_t arms, mask, inst, nsel, total;
+    size_t arms, mask, inst, stats, total;
 };
 
 Layout layout_for(int B, int K, int d) {
@@ -123,7 +123,7 @@ Layout layout_for(int B, int K, int d) {
     L.arms = off;  off = align_up(off + b * k * (size_t)chunks_for(d) * 16);
     L.mask = off;  off = align_up(off + b * kw * 4);
     L.inst = off;  off = align_up(off + b * (size_t)inst_words(d) * 4);
-    L.nsel = off;  off = align_up(off + b * k * 4);
+    L.stats = off; off = align_up(off + b * k * 8);
     L.total = off;
     return L;
 }
@@ -160,11 +160,23 @@ __device__ __forceinline__ float group_sum(float v) {
     return v;
 }
 
+// Parameters of the paper's pruning rules (bits 2, 4, 8 of the rule mask).
+struct Heuristics {
+    int32_t mask;          // rule bits 2 | 4 | 8 in use
+    int32_t ext_rounds, ext_min_n;
+    float ext_thr;
+    int32_t hist_after, hist_min_n;
+    float hist_kappa;
+    int32_t hist_min_arms, cascade_k;
+};
+
 struct StepArgs {
     float4 *arms;
     uint32_t *mask;
     int32_t *inst;        // [B][IW] per-instance blocks
-    int32_t *nsel;
+    int2 *stats;          // [B][K] rewards folded in, their sum (fp32 bits)
+    Heuristics h;
+    int64_t t;            // decisions made before this step
     StateHeader *hdr;
     const float *ctx;     // [B][D] or nullptr (flush)
     const float *reward;  // [B] or nullptr
@@ -205,8 +217,27 @@ __device__ inline BestPair better(BestPair a, BestPair b) {
     return a;
 }
 
+// Workgroup-wide reductions through one LDS slot per wavefront.
+template <class T, class Op>
+__device__ T block_reduce(T v, T *red, int lane, int wave, int nwave, Op op) {
+    for (int off = kWave / 2; off > 0; off >>= 1) v = op(v, __shfl_xor(v, off));
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    T out = red[0];
+    for (int w = 1; w < nwave; ++w) out = op(out, red[w]);
+    __syncthreads();
+    return out;
+}
+
+// Wavefronts per SIMD the register allocation must allow, by context dimension.
 template <int D>
-__global__ __launch_bounds__(256) void agft_step_kernel(StepArgs p) {
+struct Occupancy {
+    static constexpr int waves = D == 32 ? 3 : 7;
+};
+
+template <int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Occupancy<D>::waves)))
+void agft_step_kernel(StepArgs p) {
     using R = Rec<D>;
     constexpr int G = R::G, S = R::S;
     constexpr int NQ = (R::R + kWave - 1) / kWave;   // update-record chunks per thread (>= 64 threads)
@@ -237,6 +268,7 @@ __global__ __launch_bounds__(256) void agft_step_kernel(StepArgs p) {
     __shared__ float s_red_v[kMaxWaves];
     __shared__ int s_red_k[kMaxWaves];
     __shared__ int s_red_n[kMaxWaves];
+    __shared__ uint32_t s_mask2[kMaxWords];
 
     const bool decide = p.ctx != nullptr;
 
@@ -279,11 +311,123 @@ __global__ __launch_bounds__(256) void agft_step_kernel(StepArgs p) {
         }
     }
 
+    if (wave == 0 && lane < KW) s_mask[lane] = p.mask[(size_t)inst * KW + lane];
+
+    // The paper's pruning rules (Sec. 4.3) on the arms active at step start,
+    // with the previous decision's reward already counted.
+    if (p.h.mask != 0 && x_ok) {
+        __syncthreads();
+        const int2 *st = p.stats + (size_t)inst * K;
+        const Heuristics &h = p.h;
+        auto act0 = [&](int k) { return ((s_mask[k >> 5] >> (k & 31)) & 1u) != 0; };
+        // means to s_lcb, counts to s_ucb (as int bits); both are rewritten by the stream
+        int q = 0;
+        float qsum = 0.0f, qbest = -INFINITY;
+        for (int k = tid; k < K; k += nthr) {
+            const int2 v = st[k];
+            int n = v.x;
+            float rs = __int_as_float(v.y);
+            if (k == a_upd) {
+                n += 1;
+                rs += r;
+            }
+            const float mean = n > 0 ? rs / (float)n : 0.0f;
+            s_lcb[k] = mean;
+            s_ucb[k] = __int_as_float(n);
+            if (act0(k) && n >= h.hist_min_n) {
+                ++q;
+                qsum += mean;
+                qbest = fmaxf(qbest, mean);
+            }
+        }
+        auto fsum = [](float a, float b) { return a + b; };
+        auto fmx = [](float a, float b) { return fmaxf(a, b); };
+        auto isum = [](int a, int b) { return a + b; };
+        auto imx = [](int a, int b) { return a > b ? a : b; };
+        q = block_reduce(q, s_red_n, lane, wave, nwave, isum);
+        qsum = block_reduce(qsum, s_red_v, lane, wave, nwave, fsum);
+        qbest = block_reduce(qbest, s_red_v, lane, wave, nwave, fmx);
+        const bool hist_on = (h.mask & 4) && p.t >= h.hist_after && q >= h.hist_min_arms && q > 0;
+        float sigma = 0.0f;
+        if (hist_on) {
+            const float mu = qsum / (float)q;
+            float acc = 0.0f;
+            for (int k = tid; k < K; k += nthr) {
+                const int n = __float_as_int(s_ucb[k]);
+                if (act0(k) && n >= h.hist_min_n) acc += (s_lcb[k] - mu) * (s_lcb[k] - mu);
+            }
+            acc = block_reduce(acc, s_red_v, lane, wave, nwave, fsum);
+            sigma = sqrtf(acc / (float)q);
+        }
+        auto gone = [&](int k) {
+            if (!act0(k)) return false;
+            const int n = __float_as_int(s_ucb[k]);
+            const float mean = s_lcb[k];
+            if ((h.mask & 2) && p.t < h.ext_rounds && n >= h.ext_min_n && mean < h.ext_thr) return true;
+            if (hist_on && n >= h.hist_min_n && h.hist_kappa * sigma - (qbest - mean) < 0.0f) return true;
+            return false;
+        };
+        int kstar = -1;
+        if (h.mask & 8) {
+            for (int k = tid; k < K; k += nthr)
+                if (k < h.cascade_k && gone(k)) kstar = k > kstar ? k : kstar;
+            kstar = block_reduce(kstar, s_red_n, lane, wave, nwave, imx);
+        }
+        int left = 0;
+        for (int base = 0; base < K; base += nthr) {
+            const int k = base + tid;
+            const bool stay = k < K && act0(k) && !gone(k) && !(k < kstar);
+            left += stay ? 1 : 0;
+            const unsigned long long bal = __ballot(stay);
+            const int w0 = (base + wave * kWave) >> 5;
+            if (lane == 0 && w0 < KW) s_mask2[w0] = (uint32_t)(bal & 0xffffffffull);
+            if (lane == 0 && w0 + 1 < KW) s_mask2[w0 + 1] = (uint32_t)(bal >> 32);
+        }
+        left = block_reduce(left, s_red_n, lane, wave, nwave, isum);
+        if (left == 0) {
+            // keep the best mean reward among the arms that had rewards, else the first arm
+            BestPair bk{-INFINITY, 0x7fffffff};
+            int first = 0x7fffffff;
+            for (int k = tid; k < K; k += nthr)
+                if (act0(k)) {
+                    first = k < first ? k : first;
+                    if (__float_as_int(s_ucb[k]) > 0) bk = better(bk, BestPair{s_lcb[k], k});
+                }
+            for (int off = kWave / 2; off > 0; off >>= 1) {
+                BestPair o{__shfl_xor(bk.v, off), __shfl_xor(bk.k, off)};
+                bk = better(bk, o);
+                const int of = __shfl_xor(first, off);
+                first = of < first ? of : first;
+            }
+            if (lane == 0) {
+                s_red_v[wave] = bk.v;
+                s_red_k[wave] = bk.k;
+                s_red_n[wave] = first;
+            }
+            __syncthreads();
+            if (tid == 0) {
+                BestPair all{s_red_v[0], s_red_k[0]};
+                int f0 = s_red_n[0];
+                for (int w = 1; w < nwave; ++w) {
+                    all = better(all, BestPair{s_red_v[w], s_red_k[w]});
+                    f0 = s_red_n[w] < f0 ? s_red_n[w] : f0;
+                }
+                const int keep = all.k != 0x7fffffff ? all.k : f0;
+                if (keep < K) s_mask2[keep >> 5] |= 1u << (keep & 31);
+            }
+        }
+        __syncthreads();
+        if (wave == 0 && lane < KW) {
+            const uint32_t w = s_mask2[lane];
+            if (w != s_mask[lane]) p.mask[(size_t)inst * KW + lane] = w;
+            s_mask[lane] = w;
+        }
+        __syncthreads();
+    }
+
     // Active arms other than the one being updated, in index order.
     if (wave == 0) {
-        const uint32_t w = lane < KW ? p.mask[(size_t)inst * KW + lane] : 0u;
-        if (lane < KW) s_mask[lane] = w;
-        uint32_t wl = w;
+        uint32_t wl = lane < KW ? s_mask[lane] : 0u;
         if (x_ok && a_upd >= 0 && (a_upd >> 5) == lane) wl &= ~(1u << (a_upd & 31));
         if (!x_ok) wl = 0u;
         const int cnt = __popc(wl);
@@ -430,7 +574,11 @@ __global__ __launch_bounds__(256) void agft_step_kernel(StepArgs p) {
             }
             dst[c] = make_float4(v[0], v[1], v[2], v[3]);
         }
-        if (tid == 0) p.nsel[(size_t)inst * K + a_upd] += 1;
+        if (tid == 0) {
+            int2 &sa = p.stats[(size_t)inst * K + a_upd];
+            const int2 v = sa;
+            sa = make_int2(v.x + 1, __float_as_int(__int_as_float(v.y) + r));
+        }
         if (x_ok && wave == 0) {
             // score the updated arm on x_t from LDS, in the streaming order
             float f[4 * S];
@@ -560,7 +708,7 @@ struct InitArgs {
     float4 *arms;
     uint32_t *mask;
     int32_t *inst;
-    int32_t *nsel;
+    int2 *stats;
     StateHeader *hdr;
     StateHeader h;
     int32_t B, K, KW, d, C, IW;
@@ -593,7 +741,7 @@ __global__ void agft_init_kernel(InitArgs p) {
         const int rem = p.K - 32 * w;
         p.mask[idx] = rem >= 32 ? 0xffffffffu : ((1u << rem) - 1u);
     }
-    for (size_t idx = gtid; idx < (size_t)p.B * p.K; idx += gsz) p.nsel[idx] = 0;
+    for (size_t idx = gtid; idx < (size_t)p.B * p.K; idx += gsz) p.stats[idx] = make_int2(0, 0);
     for (size_t idx = gtid; idx < (size_t)p.B * p.IW; idx += gsz) {
         const int w = (int)(idx % p.IW);
         p.inst[idx] = w == kInstAprev ? -1 : (w == kInstKact ? p.K : 0);
@@ -650,8 +798,14 @@ bool config_ok(const agft_config *c) {
     if (!std::isfinite(c->lambda) || !(c->lambda > 0.0f)) return false;
     if (!std::isfinite(c->alpha0) || c->alpha0 < 0.0f) return false;
     if (c->alpha_sched != 0 && c->alpha_sched != 1) return false;
-    if (c->prune_rule != 0 && c->prune_rule != 1) return false;
+    if (c->prune_rule < 0 || c->prune_rule > 15) return false;
     if (c->prune_period < 1) return false;
+    if ((c->prune_rule & 2) && (c->ext_rounds < 0 || c->ext_min_n < 1 || !std::isfinite(c->ext_thr)))
+        return false;
+    if ((c->prune_rule & 4) && (c->hist_after < 0 || c->hist_min_n < 1 || c->hist_min_arms < 1 ||
+                                !std::isfinite(c->hist_kappa) || c->hist_kappa < 0.0f))
+        return false;
+    if ((c->prune_rule & 8) && (c->cascade_k < 0 || c->cascade_k > c->K)) return false;
     if ((c->flags & ~AGFT_ADOPT_STATE) != 0) return false;
     return true;
 }
@@ -734,7 +888,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     a.arms = at<float4>(h->base, lay.arms);
     a.mask = at<uint32_t>(h->base, lay.mask);
     a.inst = at<int32_t>(h->base, lay.inst);
-    a.nsel = at<int32_t>(h->base, lay.nsel);
+    a.stats = at<int2>(h->base, lay.stats);
     a.hdr = at<StateHeader>(h->base, 0);
     a.h = want;
     a.B = cfg->B;
@@ -766,7 +920,17 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.arms = at<float4>(h->base, h->lay.arms);
     p.mask = at<uint32_t>(h->base, h->lay.mask);
     p.inst = at<int32_t>(h->base, h->lay.inst);
-    p.nsel = at<int32_t>(h->base, h->lay.nsel);
+    p.stats = at<int2>(h->base, h->lay.stats);
+    p.h.mask = c.prune_rule & 14;
+    p.h.ext_rounds = c.ext_rounds;
+    p.h.ext_min_n = c.ext_min_n;
+    p.h.ext_thr = c.ext_thr;
+    p.h.hist_after = c.hist_after;
+    p.h.hist_min_n = c.hist_min_n;
+    p.h.hist_kappa = c.hist_kappa;
+    p.h.hist_min_arms = c.hist_min_arms;
+    p.h.cascade_k = c.cascade_k;
+    p.t = h->t;
     p.hdr = at<StateHeader>(h->base, 0);
     p.ctx = d_ctx;
     p.reward = d_reward;
@@ -778,7 +942,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.IW = inst_words(c.d);
     p.apply_update = h->pending;
     const int64_t t = h->t;
-    p.prune_now = (d_ctx != nullptr && c.prune_rule == 1 && t > 0 && t % c.prune_period == 0) ? 1 : 0;
+    p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
     const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves_for(c.K, c.d)));
@@ -812,7 +976,7 @@ int agft_get_state(const agft_handle *h, agft_state_view *out) {
     out->mask = at<uint32_t>(h->base, h->lay.mask);
     out->inst = at<int32_t>(h->base, h->lay.inst);
     out->inst_words = inst_words(h->cfg.d);
-    out->nsel = at<int32_t>(h->base, h->lay.nsel);
+    out->stats = at<int32_t>(h->base, h->lay.stats);
     return AGFT_OK;
 }
 

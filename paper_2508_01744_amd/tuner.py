@@ -19,13 +19,16 @@ class Tuner:
     """B independent AGFT frequency tuners (disjoint LinUCB over K arms, Sec. 4.2)."""
 
     def __init__(self, B, K, d, lam=1.0, alpha0=1.0, alpha_sched=0, prune_rule=0,
-                 prune_period=50, device="cuda", stream=None, state=None, adopt=False):
+                 prune_period=50, device="cuda", stream=None, state=None, adopt=False,
+                 heuristics=None):
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
         self.cfg = L.agft_config(int(B), int(K), int(d), float(lam), float(alpha0),
                                  int(alpha_sched), int(prune_rule), int(prune_period),
                                  L.AGFT_ADOPT_STATE if adopt else 0)
+        for name, value in (heuristics or {}).items():
+            setattr(self.cfg, name, value)
         self.nbytes = L.agft_state_bytes(self.cfg)
         if self.nbytes == 0:
             raise ValueError("invalid tuner configuration")
@@ -48,11 +51,14 @@ class Tuner:
     @classmethod
     def from_workload(cls, wl, B=None, **kw):
         return cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0, wl.alpha_sched,
-                   wl.prune, wl.period, **kw)
+                   wl.prune, wl.period, heuristics=wl.heuristics(), **kw)
 
     def close(self):
         if getattr(self, "h", None):
-            L.agft_destroy(self.h)
+            try:
+                L.agft_destroy(self.h)
+            except TypeError:      # interpreter shutdown: ctypes already torn down
+                pass
             self.h = None
 
     def __del__(self):
@@ -111,7 +117,7 @@ class Tuner:
             inst=inst,
             aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2],
             xprev=inst[:, 4:4 + d].view(torch.float32),
-            nsel=region(v.nsel, B * K, torch.int32, (B, K)),
+            stats=region(v.stats, B * K * 2, torch.int32, (B, K, 2)),
         )
 
     @property

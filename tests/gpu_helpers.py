@@ -20,7 +20,7 @@ def run_open_loop(cfg, X, R, flush=True):
     T, B, d = X.shape
     dev = torch.device("cuda")
     tuner = Tuner(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
-                  cfg["prune"], cfg["period"], device=dev)
+                  cfg["prune"], cfg["period"], device=dev, heuristics=cfg.get("heuristics"))
     Xd = torch.as_tensor(np.asarray(X, dtype=np.float32), device=dev)
     Rd = torch.as_tensor(np.asarray(R, dtype=np.float32), device=dev)
     K, KW = cfg["K"], (cfg["K"] + 31) // 32

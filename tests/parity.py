@@ -33,16 +33,32 @@ class ParityError(AssertionError):
 
 
 class Checker:
-    def __init__(self, name, K, ids, g_a, g_keep, g_s=None, g_x=None, g_r=None):
+    def __init__(self, name, K, ids, g_a, g_keep, g_s=None, g_x=None, g_r=None, rules=0,
+                 cascade_k=0):
         self.name, self.K, self.ids = name, K, list(ids)
         self.g_a, self.g_keep, self.g_s, self.g_x, self.g_r = g_a, g_keep, g_s, g_x, g_r
+        self.rules, self.cascade_k = rules, cascade_k
         self.st = dict(max_score_err=0.0, max_ctx_err=0.0, max_reward_err=0.0, forced=0,
-                       forced_prune=0, exact_tie_steps=0, decisions=0, no_decision=0)
+                       forced_prune=0, forced_rules=0, exact_tie_steps=0, decisions=0,
+                       no_decision=0)
 
     def fail(self, msg):
         raise ParityError(f"{self.name}: {msg}")
 
-    def __call__(self, t, x, r_prev, ucb, lcb, keep, action):
+    def _rules_ambiguous(self, margins, k):
+        """Arm k's removal by the paper's rules (bits 2, 4, 8) could go either
+        way: its own comparison, or that of a higher arm whose cascade covers
+        it, sits within TIE of the threshold."""
+        if margins is None:
+            return False
+        if margins[k] <= TIE:
+            return True
+        if self.rules & 8:
+            hi = np.arange(self.K)
+            return bool(np.any((hi > k) & (hi < self.cascade_k) & (margins <= TIE)))
+        return False
+
+    def __call__(self, t, x, r_prev, ucb, lcb, keep, action, margins=None):
         st, ids = self.st, self.ids
         if self.g_x is not None:
             ex = np.abs(self.g_x[t] - x) / np.maximum(1.0, np.abs(x))
@@ -57,20 +73,31 @@ class Checker:
             if er.max() > ENV_TOL:
                 self.fail(f"reward mismatch at t={t - 1}: max rel err {er.max():.3e}")
         act = np.isfinite(ucb)
-        if self.g_s is not None:
-            if not np.array_equal(np.isfinite(self.g_s[t, :, 0]), act):
-                self.fail(f"active sets differ at t={t}")
-            for row, ref in ((0, ucb), (1, lcb)):
-                err = np.where(act, np.abs(self.g_s[t, :, row] - ref) / np.maximum(1.0, np.abs(ref)), 0.0)
-                st["max_score_err"] = max(st["max_score_err"], float(err.max()))
-                if err.max() > SCORE_TOL:
-                    i, k = np.unravel_index(int(np.argmax(err)), err.shape)
-                    self.fail(f"score mismatch at t={t}, instance {ids[i]}, arm {k}: "
-                              f"{self.g_s[t, i, row, k]!r} vs {ref[i, k]!r}")
         commit_keep = keep.copy()
         commit_a = action.copy()
         for i in range(len(ids)):
             ga = int(self.g_a[t, i])
+            if self.g_s is not None:
+                g_act = np.isfinite(self.g_s[t, i, 0])
+                if not np.array_equal(g_act, act[i]):
+                    diff = np.flatnonzero(g_act != act[i])
+                    if not all(self._rules_ambiguous(None if margins is None else margins[i], k)
+                               for k in diff):
+                        self.fail(f"active sets differ at t={t}, instance {ids[i]}, arms {diff}")
+                    # a near-threshold pruning rule decided differently: take the GPU's set
+                    st["forced_rules"] += 1
+                    commit_keep[i] = self.g_keep[t, i]
+                    commit_a[i] = ga
+                    continue
+                for row, ref in ((0, ucb[i]), (1, lcb[i])):
+                    with np.errstate(invalid="ignore"):
+                        err = np.where(act[i], np.abs(self.g_s[t, i, row] - ref) / np.maximum(1.0, np.abs(ref)),
+                                       0.0)
+                    st["max_score_err"] = max(st["max_score_err"], float(err.max()))
+                    if err.max() > SCORE_TOL:
+                        k = int(np.argmax(err))
+                        self.fail(f"score mismatch at t={t}, instance {ids[i]}, arm {k}: "
+                                  f"{self.g_s[t, i, row, k]!r} vs {ref[k]!r}")
             if action[i] < 0:
                 st["no_decision"] += 1
                 if ga != -1:
@@ -117,8 +144,9 @@ def compare(wl, T, probes, rec):
     chk = Checker(wl.name, wl.K, probes, rec["a"].numpy(),
                   mask_words_to_bool(rec["mask"].numpy(), wl.K),
                   rec["scores"].numpy().astype(np.float64) if "scores" in rec else None,
-                  rec["x"].numpy().astype(np.float64), rec["r"].numpy().astype(np.float64))
-    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk)
+                  rec["x"].numpy().astype(np.float64), rec["r"].numpy().astype(np.float64),
+                  rules=wl.prune, cascade_k=wl.cascade_k)
+    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14))
     st = chk.finish()
     st["oracle"] = out["oracle"]
     return st
@@ -132,11 +160,15 @@ def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s):
     T = X.shape[0]
     ora = Oracle(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
                  cfg["prune"], cfg["period"])
-    chk = Checker(name, cfg["K"], range(cfg["B"]), g_a, mask_words_to_bool(g_masks, cfg["K"]), g_s)
+    heur = cfg.get("heuristics")
+    if heur:
+        ora.set_heuristics(**heur)
+    chk = Checker(name, cfg["K"], range(cfg["B"]), g_a, mask_words_to_bool(g_masks, cfg["K"]), g_s,
+                  rules=cfg["prune"], cascade_k=(heur or {}).get("cascade_k", 0))
     r_prev = None
     for t in range(T):
-        ucb, lcb, keep, action = ora.decide(X[t], r_prev)
-        a, k = chk(t, X[t], r_prev, ucb, lcb, keep, action)
+        ucb, lcb, keep, action, marg = ora.decide(X[t], r_prev, margins=True)
+        a, k = chk(t, X[t], r_prev, ucb, lcb, keep, action, marg)
         ora.commit(X[t], a, k)
         r_prev = R[t]
     ora.flush(r_prev)

@@ -50,6 +50,9 @@ def _cfg(**kw):
 def test_state_bytes(lib):
     n = L.agft_state_bytes(_cfg())
     assert n > 0 and n % 256 == 0
+    good = dict(prune_rule=15, ext_rounds=60, ext_min_n=3, ext_thr=-1.2, hist_after=30, hist_min_n=6,
+                hist_kappa=1.0, hist_min_arms=3, cascade_k=16)
+    assert L.agft_state_bytes(_cfg(**good)) == n
     # the arm records dominate: B * K * (d/2) * ((d+6)/4) float4 chunks
     # (d + d(d+1)/2 floats per arm, padded to whole chunks per lane slice)
     for d, chunks in ((8, 12), (16, 40), (32, 144)):
@@ -58,7 +61,11 @@ def test_state_bytes(lib):
         assert 4096 * 128 * chunks * 16 <= big < 4096 * 128 * chunks * 16 * 1.05
     for bad in (dict(B=0), dict(K=0), dict(K=1025), dict(lambda_=0.0), dict(lambda_=float("nan")),
                 dict(alpha0=-1.0), dict(alpha0=float("inf")), dict(alpha_sched=2),
-                dict(prune_rule=3), dict(prune_period=0), dict(flags=4), dict(d=12)):
+                dict(prune_rule=16), dict(prune_rule=-1), dict(prune_period=0), dict(flags=4), dict(d=12),
+                dict(prune_rule=2, ext_min_n=0), dict(prune_rule=2, ext_min_n=3, ext_thr=float("nan")),
+                dict(prune_rule=4, hist_min_n=0, hist_min_arms=3),
+                dict(prune_rule=4, hist_min_n=6, hist_min_arms=3, hist_kappa=-1.0),
+                dict(prune_rule=8, cascade_k=17)):
         assert L.agft_state_bytes(_cfg(**bad)) == 0, bad
 
 

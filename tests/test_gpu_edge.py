@@ -15,7 +15,8 @@ pytestmark = pytest.mark.gpu
 
 
 def _cfg(B, K, d, lam=1.0, alpha0=0.5, sched=0, prune=0, period=50):
-    return dict(B=B, K=K, d=d, lam=lam, alpha0=alpha0, sched=sched, prune=prune, period=period)
+    return dict(B=B, K=K, d=d, lam=lam, alpha0=alpha0, sched=sched, prune=prune, period=period,
+                heuristics=None)
 
 
 def _open_loop_case(name, cfg, T, seed, scale=1.0):
@@ -83,7 +84,7 @@ def test_missing_reward_and_flush():
     tuner.flush(r[1])
     v = tuner.view()
     torch.cuda.synchronize()
-    assert int(v["nsel"].sum()) == 8 and v["pending"] == 0
+    assert int(v["stats"][..., 0].sum()) == 8 and v["pending"] == 0
     assert (v["aprev"].cpu() == -1).all()
     tuner.step(x[2])          # no reward needed after a flush
     torch.cuda.synchronize()
@@ -169,3 +170,21 @@ def test_determinism():
     for key in a["probes"]:
         assert torch.equal(a["probes"][key], b["probes"][key]), key
     assert torch.equal(a["tuner"].state, b["tuner"].state)
+
+
+AGGRESSIVE = dict(ext_rounds=40, ext_min_n=1, ext_thr=-1.0, hist_after=10, hist_min_n=2,
+                  hist_kappa=0.5, hist_min_arms=3)
+
+
+@pytest.mark.parametrize("d,K,rules", [(8, 20, 2 | 8), (16, 70, 4), (16, 40, 15), (32, 33, 14),
+                                       (8, 1024, 15)])
+def test_paper_pruning_rules(d, K, rules):
+    """The paper's extreme/historical/cascade rules (Sec. 4.3) with thresholds
+    set so that they fire often, against the oracle (open loop)."""
+    cfg = _cfg(6, K, d, alpha0=0.6, prune=rules, period=25)
+    cfg["heuristics"] = dict(AGGRESSIVE, cascade_k=K // 2)
+    T = 120 if K < 1024 else 60
+    st, a, tuner = _open_loop_case(f"rules={rules} d={d} K={K}", cfg, T, 100 + K)
+    kact = tuner.view()["kact"].cpu().numpy()
+    assert (kact >= 1).all() and (kact < K).any()
+    say(f"[edge] rules forced {st['forced_rules']}")

@@ -29,7 +29,8 @@ def _run_and_compare(wl, probes):
     wth, wai = compare_model(out["tuner"], st["oracle"], probes, THETA_TOL, AINV_TOL)
     say(f"[parity] {wl.name}: max score err {st['max_score_err']:.2e}, ctx err "
         f"{st['max_ctx_err']:.2e}, reward err {st['max_reward_err']:.2e}, forced "
-        f"{st['forced']}/{st['decisions']}, prune forced {st['forced_prune']}, exact-tie steps "
+        f"{st['forced']}/{st['decisions']}, prune forced {st['forced_prune']}, rules forced "
+        f"{st['forced_rules']}, exact-tie steps "
         f"{st['exact_tie_steps']}, theta err {wth:.2e}, Ainv err {wai:.2e}")
     return st
 
@@ -42,6 +43,22 @@ def test_small_every_instance(cfg):
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
 def test_full_size_probes(cfg):
+    wl = get_workload(cfg)
+    _run_and_compare(wl, probe_instances(wl.B, 64))
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("cfg", ["cfg2p", "cfg3p", "cfg4p", "cfg5p"])
+def test_small_paper_pruning(cfg):
+    """The workloads with the paper's pruning rules added (Sec. 4.3)."""
+    small = {"cfg2p": dict(B=32, T=400), "cfg3p": dict(B=16, T=300), "cfg4p": dict(B=24, T=300),
+             "cfg5p": dict(B=8, T=300)}
+    wl = get_workload(cfg, **small[cfg])
+    _run_and_compare(wl, list(range(wl.B)))
+
+
+@pytest.mark.parametrize("cfg", ["cfg2p", "cfg4p"])
+def test_full_size_paper_pruning(cfg):
     wl = get_workload(cfg)
     _run_and_compare(wl, probe_instances(wl.B, 64))
     torch.cuda.empty_cache()
