@@ -43,6 +43,14 @@ class Workload:
     hist_min_n: int = 6
     hist_kappa: float = 1.0
     hist_min_arms: int = 3
+    # switch to greedy exploitation once a Page-Hinkley test finds the reward
+    # sequence stable (Sec. 4.2, Eq. 2); the paper names the test but none of
+    # its constants, except a maturity threshold of 100 rounds (Sec. 4.4)
+    exploit: int = 0
+    ph_delta: float = 0.05
+    ph_lambda: float = 5.0
+    ph_window: int = 100
+    ph_min_rounds: int = 100
 
     @property
     def arm_record_floats(self) -> int:
@@ -59,6 +67,10 @@ class Workload:
                     hist_after=self.hist_after, hist_min_n=self.hist_min_n,
                     hist_kappa=self.hist_kappa, hist_min_arms=self.hist_min_arms,
                     cascade_k=self.cascade_k)
+
+    def page_hinkley(self) -> dict:
+        return dict(ph_delta=self.ph_delta, ph_lambda=self.ph_lambda, ph_window=self.ph_window,
+                    ph_min_rounds=self.ph_min_rounds)
 
     def alpha_at(self, t: int) -> float:
         if self.alpha_sched == 0:
@@ -99,16 +111,30 @@ def with_paper_pruning(wl: Workload) -> Workload:
     return Workload(**d)
 
 
+def with_exploitation(wl: Workload) -> Workload:
+    """The same workload with the Page-Hinkley switch to greedy exploitation."""
+    d = dict(wl.__dict__)
+    d["exploit"] = 1
+    d["name"] = wl.name + "e"
+    d["description"] = wl.description + ", plus the switch to greedy exploitation"
+    return Workload(**d)
+
+
 def get_workload(cfg, **overrides) -> Workload:
     """Workload by id (1..5) or name ("cfg4"), optionally with fields replaced
     (smaller B or T for quick parity cases)."""
-    paper = False
+    suffix = ""
     if isinstance(cfg, str):
-        paper = cfg.endswith("p")
-        cfg = int(cfg.replace("cfg", "").rstrip("p"))
+        body = cfg.replace("cfg", "")
+        suffix = body.lstrip("0123456789")
+        cfg = int(body[:len(body) - len(suffix)])
+        if set(suffix) - set("pe"):
+            raise ValueError(f"unknown workload suffix {suffix!r} (p: paper pruning, e: exploitation)")
     wl = WORKLOADS[cfg]
-    if paper:
+    if "p" in suffix:
         wl = with_paper_pruning(wl)
+    if "e" in suffix:
+        wl = with_exploitation(wl)
     if overrides:
         d = dict(wl.__dict__)
         d.update(overrides)

@@ -44,6 +44,17 @@
  * pivoting each time A_k changes; theta_k is then recomputed as A_k^{-1} b_k.
  * There is no rank-1 identity here: that is the GPU path's business.
  *
+ * Exploitation (Sec. 4.2, Eq. 2), when enabled: each reward folded in also
+ * feeds a two-sided Page-Hinkley test on the instance's reward sequence
+ * (running mean rbar_n; m+ += r - rbar_n - delta, m- += rbar_n - r - delta;
+ * an alarm when m+ - min m+ or m- - min m- exceeds lambda, after which the
+ * test restarts).  The sequence counts as stable once t >= min_rounds and no
+ * alarm was raised in the last `window` rounds; from then on the instance
+ * exploits for good: a_t = argmax over the active arms of theta_k^T x_t
+ * (reported as both UCB and LCB), rule 1 is not applied, updates go on.
+ * The test decides an integer (the switch round), so it runs in single
+ * precision with the GPU kernel's operation order; the model stays double.
+ *
  * Step order: the reward r_{t-1} of the previous decision arrives with the
  * next context, so ora_decide first applies Eq. 3-5 to the arm chosen at
  * t-1 with (x_{t-1}, r_{t-1}), then scores x_t, prunes and picks a_t.
@@ -70,6 +81,13 @@ typedef struct {
     /* parameters of rules 2-8 */
     int ext_rounds, ext_min_n, hist_after, hist_min_n, hist_min_arms, cascade_k;
     double ext_thr, hist_kappa;
+    /* exploitation switch (Page-Hinkley, single precision) */
+    int exploit, ph_window, ph_min_rounds;
+    float ph_delta, ph_lambda;
+    float *ph;              /* [B][6]        n, mean, m+, min m+, m-, min m- */
+    float *ph_margin;       /* [B]           lambda - larger statistic at the last test */
+    long *ph_last;          /* [B]           round of the last alarm (0 at start) */
+    long *mode;             /* [B]           -1 exploring, else the round exploitation began */
     double *A;              /* [B][K][d][d]  Eq. 3 */
     double *b;              /* [B][K][d]     Eq. 4 */
     double *Ainv;           /* [B][K][d][d]  inverse of A */
@@ -120,6 +138,8 @@ static int gauss_jordan_inverse(int d, const double *M, double *out)
 void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, double *lcb,
                    unsigned char *keep, int *action, double *margins);
 void ora_get_rsum(const void *h, int i, double *rsum);
+void ora_set_exploit(void *h, int on, double delta, double lambda, int window, int min_rounds);
+void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, long *mode);
 
 static int all_finite(const double *v, int n)
 {
@@ -148,10 +168,15 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
     o->xprev = (double *)calloc((size_t)B * d, sizeof(double));
     o->aprev = (int *)malloc((size_t)B * sizeof(int));
     o->bad = (int *)calloc((size_t)B, sizeof(int));
+    o->ph = (float *)calloc((size_t)B * 6, sizeof(float));
+    o->ph_margin = (float *)malloc((size_t)B * sizeof(float));
+    o->ph_last = (long *)calloc((size_t)B, sizeof(long));
+    o->mode = (long *)malloc((size_t)B * sizeof(long));
     if (!o->A || !o->b || !o->Ainv || !o->theta || !o->active || !o->nsel || !o->rsum ||
-        !o->xprev || !o->aprev || !o->bad) {
+        !o->xprev || !o->aprev || !o->bad || !o->ph || !o->ph_margin || !o->ph_last || !o->mode) {
         free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
-        free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+        free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad);
+        free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o);
         return NULL;
     }
     /* A_k(0) = lambda I, b_k(0) = 0, hence A_k^{-1}(0) = I / lambda, theta_k(0) = 0. */
@@ -161,7 +186,11 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
             o->Ainv[(k * d + r) * d + r] = 1.0 / lambda;
         }
     memset(o->active, 1, nk);
-    for (int i = 0; i < B; ++i) o->aprev[i] = -1;
+    for (int i = 0; i < B; ++i) {
+        o->aprev[i] = -1;
+        o->mode[i] = -1;
+        o->ph_margin[i] = INFINITY;
+    }
     return o;
 }
 
@@ -170,7 +199,49 @@ void ora_destroy(void *h)
     ora_t *o = (ora_t *)h;
     if (!o) return;
     free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
-    free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad); free(o);
+    free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad);
+    free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o);
+}
+
+/* Exploitation switch: on/off and the Page-Hinkley parameters (see the header). */
+void ora_set_exploit(void *h, int on, double delta, double lambda, int window, int min_rounds)
+{
+    ora_t *o = (ora_t *)h;
+    o->exploit = on;
+    o->ph_delta = (float)delta;
+    o->ph_lambda = (float)lambda;
+    o->ph_window = window;
+    o->ph_min_rounds = min_rounds;
+}
+
+/* One reward into instance i's Page-Hinkley test at round t (single precision). */
+static void page_hinkley(ora_t *o, int i, long t, double reward)
+{
+    float *s = o->ph + (size_t)i * 6;
+    const float r = (float)reward;
+    s[0] = s[0] + 1.0f;
+    s[1] = s[1] + (r - s[1]) / s[0];
+    s[2] = s[2] + (r - s[1] - o->ph_delta);
+    s[3] = fminf(s[3], s[2]);
+    s[4] = s[4] + (s[1] - r - o->ph_delta);
+    s[5] = fminf(s[5], s[4]);
+    const float up = s[2] - s[3], down = s[4] - s[5];
+    o->ph_margin[i] = o->ph_lambda - (up > down ? up : down);
+    if (up > o->ph_lambda || down > o->ph_lambda) {
+        o->ph_last[i] = t;
+        for (int q = 0; q < 6; ++q) s[q] = 0.0f;
+    }
+}
+
+/* Page-Hinkley state of instance i: stats[6] (n, mean, m+, min m+, m-, min m-),
+ * the last margin, the last alarm round and the mode; outputs may be NULL. */
+void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, long *mode)
+{
+    const ora_t *o = (const ora_t *)h;
+    if (stats) memcpy(stats, o->ph + (size_t)i * 6, sizeof(float) * 6);
+    if (margin) *margin = o->ph_margin[i];
+    if (last) *last = o->ph_last[i];
+    if (mode) *mode = o->mode[i];
 }
 
 /* Parameters of pruning rules 2-8 (see the header). */
@@ -274,6 +345,7 @@ static void apply_pending(ora_t *o, int i, const double *r)
     if (a < 0) return;
     if (r == NULL || !isfinite(r[i])) { o->bad[i] += 1; return; }
     update_arm(o, i, a, o->xprev + (size_t)i * o->d, r[i]);
+    if (o->exploit && o->mode[i] < 0) page_hinkley(o, i, o->t, r[i]);
 }
 
 double ora_alpha(const void *h, long t)
@@ -330,6 +402,9 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
             for (int k = 0; k < K; ++k) kp[k] = act[k];
         }
         if (margins) memcpy(margins + (size_t)i * K, marg, sizeof(double) * K);
+        if (o->exploit && o->mode[i] < 0 && t >= o->ph_min_rounds && t - o->ph_last[i] >= o->ph_window)
+            o->mode[i] = t;
+        const int greedy = o->mode[i] >= 0;
         for (int k = 0; k < K; ++k) {
             if (!act[k]) continue;
             size_t ik = (size_t)i * K + k;
@@ -342,10 +417,10 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
                 quad += xi[p] * row;
             }
             double w = sqrt(quad > 0.0 ? quad : 0.0);
-            U[k] = m + alpha * w;
-            L[k] = m - alpha * w;
+            U[k] = greedy ? m : m + alpha * w;   /* Eq. 2 when exploiting, else Eq. 1 */
+            L[k] = greedy ? m : m - alpha * w;
         }
-        if (prune_now) {
+        if (prune_now && !greedy) {
             double lstar = -INFINITY;
             for (int k = 0; k < K; ++k)
                 if (act[k] && L[k] > lstar) lstar = L[k];

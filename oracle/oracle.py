@@ -33,6 +33,8 @@ def _declare(lib):
     lib.ora_decide_ex.argtypes = [P, P, P, P, P, P, P, P]
     lib.ora_set_heuristics.argtypes = [P, I, I, D, I, I, D, I, I]
     lib.ora_get_rsum.argtypes = [P, I, P]
+    lib.ora_set_exploit.argtypes = [P, I, D, D, I, I]
+    lib.ora_get_ph.argtypes = [P, I, P, P, P, P]
     lib.ora_commit.argtypes = [P, P, P, P]
     lib.ora_flush.argtypes = [P, P]
     lib.ora_get.argtypes = [P, I, P, P, P, P, P, P, P]
@@ -79,7 +81,24 @@ class Oracle:
                 wl.alpha_sched, wl.prune, wl.period, lib=lib)
         if wl.prune & 14:
             o.set_heuristics(**wl.heuristics())
+        if wl.exploit:
+            o.set_exploit(True, **wl.page_hinkley())
         return o
+
+    def set_exploit(self, on, ph_delta, ph_lambda, ph_window, ph_min_rounds):
+        """Page-Hinkley switch to greedy exploitation (Sec. 4.2, Eq. 2)."""
+        self.lib.ora_set_exploit(self.h, int(bool(on)), float(ph_delta), float(ph_lambda),
+                                 int(ph_window), int(ph_min_rounds))
+
+    def page_hinkley(self, i):
+        """(stats[6] float32, last margin, last alarm round, mode) of instance i."""
+        stats = np.empty(6, dtype=np.float32)
+        margin = ctypes.c_float(0.0)
+        last = ctypes.c_long(0)
+        mode = ctypes.c_long(0)
+        self.lib.ora_get_ph(self.h, int(i), _ptr(stats), ctypes.byref(margin), ctypes.byref(last),
+                            ctypes.byref(mode))
+        return stats, margin.value, last.value, mode.value
 
     def set_heuristics(self, ext_rounds, ext_min_n, ext_thr, hist_after, hist_min_n, hist_kappa,
                        hist_min_arms, cascade_k):

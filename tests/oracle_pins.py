@@ -440,3 +440,99 @@ def pin_heuristics_brute_force(lib):
 
 ALL_PINS += [pin_extreme_pruning, pin_historical_pruning, pin_cascade_pruning,
              pin_heuristics_keep_one_arm, pin_heuristics_brute_force]
+
+
+# ---- Page-Hinkley switch to greedy exploitation (Sec. 4.2, Eq. 2) ----
+
+PH = dict(ph_delta=0.05, ph_lambda=5.0, ph_window=100, ph_min_rounds=100)
+
+
+def _ph_reference(rewards, delta, lam):
+    """Independent restatement of the two-sided Page-Hinkley test in float32:
+    returns the alarm rounds (reward s is folded in at round s + 1)."""
+    f = np.float32
+    alarms = []
+    n = f(0); mean = f(0); up = f(0); up_min = f(0); dn = f(0); dn_min = f(0)
+    for s, r in enumerate(np.asarray(rewards, dtype=np.float32)):
+        n = f(n + f(1))
+        mean = f(mean + f(f(r - mean) / n))
+        up = f(up + f(f(r - mean) - f(delta)))
+        up_min = min(up_min, up)
+        dn = f(dn + f(f(mean - r) - f(delta)))
+        dn_min = min(dn_min, dn)
+        if f(up - up_min) > f(lam) or f(dn - dn_min) > f(lam):
+            alarms.append(s + 1)
+            n = mean = up = up_min = dn = dn_min = f(0)
+    return alarms
+
+
+def _run_rewards(lib, rewards, K=3, d=2, ph=PH, rule=0, x_fn=None):
+    """One instance: the oracle picks its own arms, the reward of every pick
+    is scripted; returns per-round (ucb, lcb, action) and the oracle."""
+    ora = Oracle(1, K, d, 1.0, 1.0, 0, rule, 50, lib=lib)
+    ora.set_exploit(True, **ph)
+    rng = np.random.default_rng(3)
+    r_prev = None
+    hist = []
+    for t, r in enumerate(rewards):
+        x = x_fn(t, rng) if x_fn else np.concatenate([[1.0], rng.standard_normal(d - 1)])[None, :]
+        ucb, lcb, keep, action = ora.step(x, r_prev)
+        hist.append((x[0], ucb[0], lcb[0], int(action[0])))
+        r_prev = np.array([r])
+    return hist, ora
+
+
+def pin_page_hinkley_switch_round(lib):
+    """A stationary reward sequence never alarms, so exploitation starts at
+    round max(min_rounds, window); a step in the mean alarms at the round an
+    independent float32 restatement says, and postpones the switch to that
+    round plus the window."""
+    flat = [-1.0] * 160
+    hist, ora = _run_rewards(lib, flat)
+    assert ora.page_hinkley(0)[3] == 100
+    assert all(h[1][h[3]] != h[2][h[3]] for h in hist[:100])       # UCB > LCB while exploring
+    hist, ora = _run_rewards(lib, flat, ph=dict(PH, ph_min_rounds=130))
+    assert ora.page_hinkley(0)[3] == 130
+    step = [-1.0] * 80 + [-0.2] * 200
+    alarms = _ph_reference(step, 0.05, 5.0)
+    assert alarms and 80 < alarms[0] < 120
+    hist, ora = _run_rewards(lib, step)
+    _, _, last, mode = ora.page_hinkley(0)
+    expect_last = max(a for a in alarms if a < mode) if mode >= 0 else alarms[-1]
+    assert last == expect_last and mode == max(100, last + 100)
+    noisy = list(np.random.default_rng(4).normal(-1.0, 0.4, 400))
+    hist, ora = _run_rewards(lib, noisy)
+    alarms = _ph_reference(noisy, 0.05, 5.0)
+    _, _, last, mode = ora.page_hinkley(0)
+    before = [a for a in alarms if mode < 0 or a < mode]
+    assert last == (before[-1] if before else 0)
+
+
+def pin_greedy_after_switch(lib):
+    """Once exploiting, the choice is argmax theta_k^T x_t over the active arms
+    (Eq. 2, ties to the lowest index), reported as both UCB and LCB, with
+    theta_k recomputed from the arm's history by direct solve."""
+    K, d = 4, 3
+    rng = np.random.default_rng(21)
+    ora = Oracle(1, K, d, 1.0, 1.0, 0, 0, 50, lib=lib)
+    ora.set_exploit(True, ph_delta=0.05, ph_lambda=1e9, ph_window=10, ph_min_rounds=10)
+    hist = [[] for _ in range(K)]
+    r_prev = None
+    for t in range(40):
+        x = np.concatenate([[1.0], rng.standard_normal(d - 1)])
+        ucb, lcb, keep, action = ora.step(x[None, :], r_prev)
+        a = int(action[0])
+        if t >= 10:
+            m = []
+            for k in range(K):
+                A = np.eye(d) + sum((np.outer(z, z) for z, _ in hist[k]), np.zeros((d, d)))
+                b = sum((q * z for z, q in hist[k]), np.zeros(d))
+                m.append(np.linalg.solve(A, b) @ x)
+            assert np.allclose(ucb[0], m, atol=1e-12) and np.allclose(lcb[0], m, atol=1e-12)
+            assert a == max(range(K), key=lambda k: (m[k], -k))
+        r = float(rng.normal(-1.0 + 0.2 * a, 0.1))
+        hist[a].append((x, r))
+        r_prev = np.array([r])
+
+
+ALL_PINS += [pin_page_hinkley_switch_round, pin_greedy_after_switch]

@@ -17,7 +17,7 @@ MUTANTS = {
     "eq4_wrong_sign": ("b[p] += r * x[p];", "b[p] -= r * x[p];"),
     "eq5_transposed_index": ("s += Ainv[p * d + q] * b[q];", "s += Ainv[p * d + q] * b[p];"),
     "score_wrong_operand": ("row += Ainv[p * d + q] * xi[q];", "row += Ainv[p * d + q] * xi[p];"),
-    "lcb_wrong_sign": ("L[k] = m - alpha * w;", "L[k] = m + alpha * w;"),
+    "lcb_wrong_sign": ("L[k] = greedy ? m : m - alpha * w;", "L[k] = greedy ? m : m + alpha * w;"),
     "ties_to_highest_index": ("(best < 0 || U[k] > U[best])", "(best < 0 || U[k] >= U[best])"),
     "prune_non_strict": ("if (act[k] && U[k] < lstar) kp[k] = 0;",
                          "if (act[k] && U[k] <= lstar) kp[k] = 0;"),
@@ -44,6 +44,12 @@ MUTANTS = {
                                     "if (gone[k] && k <= o->cascade_k) kstar = k;"),
     "keep_one_worst_mean": ("(n[keep] == 0 || mean[k] > mean[keep])", "(n[keep] == 0 || mean[k] < mean[keep])"),
     "reward_sum_not_kept": ("    o->rsum[ik] += r;", "    o->rsum[ik] += 0.0 * r;"),
+    "ph_drift_sign": ("s[2] = s[2] + (r - s[1] - o->ph_delta);", "s[2] = s[2] + (r - s[1] + o->ph_delta);"),
+    "ph_minimum_not_tracked": ("s[3] = fminf(s[3], s[2]);", "s[3] = s[2];"),
+    "ph_no_restart": ("        for (int q = 0; q < 6; ++q) s[q] = 0.0f;\n", ""),
+    "ph_window_off_by_one": ("t - o->ph_last[i] >= o->ph_window", "t - o->ph_last[i] > o->ph_window"),
+    "ph_min_rounds_ignored": ("t >= o->ph_min_rounds && ", ""),
+    "greedy_scores_with_bonus": ("U[k] = greedy ? m : m + alpha * w;", "U[k] = m + alpha * w;"),
 }
 
 
