@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define AGFT_ABI_VERSION 1
+#define AGFT_ABI_VERSION 2
 
 enum agft_status {
     AGFT_OK = 0,
@@ -92,6 +92,19 @@ typedef struct agft_config {
     float hist_kappa;      /* finite, >= 0 */
     int32_t hist_min_arms; /* >= 1 */
     int32_t cascade_k;     /* 0..K */
+    /* switch to greedy exploitation (Sec. 4.2, Eq. 2): 0 off, 1 on.  Every
+       reward folded in feeds a two-sided Page-Hinkley test in single precision
+       (running mean rbar; m+ += (r - rbar) - ph_delta, m- += (rbar - r) - ph_delta;
+       an alarm when m+ - min m+ or m- - min m- exceeds ph_lambda, after which the
+       test restarts).  Once t >= ph_min_rounds and no alarm came in the last
+       ph_window rounds, the instance exploits for good: a_t = argmax over the
+       active arms of theta_k^T x_t (reported as both UCB and LCB), reading only
+       the theta chunk of each record; rule 1 is not applied; updates go on. */
+    int32_t exploit;
+    float ph_delta;        /* finite */
+    float ph_lambda;       /* finite, >= 0 */
+    int32_t ph_window;     /* >= 0 */
+    int32_t ph_min_rounds; /* >= 0 */
 } agft_config;
 
 typedef struct agft_handle agft_handle;
@@ -115,9 +128,12 @@ typedef struct agft_state_view {
     uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k active */
     int32_t *inst;      /* [B][inst_words] per-instance block of 32-bit words:
                            [0] last decision (-1: none), [1] number of active arms,
-                           [2] non-finite contexts or rewards met, [3] reserved,
-                           [4 .. 4+d) context of the last decision (fp32) */
-    int32_t inst_words; /* words per instance block: 4 + d rounded up to 16 */
+                           [2] non-finite contexts or rewards met,
+                           [3] -1 while exploring, else the round exploitation began,
+                           [4..9] Page-Hinkley n, mean, m+, min m+, m-, min m- (fp32),
+                           [10] round of its last alarm, [11] its last margin (fp32),
+                           [12 .. 12+d) context of the last decision (fp32) */
+    int32_t inst_words; /* words per instance block: 12 + d rounded up to 16 */
     int32_t *stats;     /* [B][K][2] per arm: [0] rewards folded in (int32),
                            [1] their sum (fp32 bits) */
 } agft_state_view;

@@ -140,6 +140,7 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
 void ora_get_rsum(const void *h, int i, double *rsum);
 void ora_set_exploit(void *h, int on, double delta, double lambda, int window, int min_rounds);
 void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, long *mode);
+void ora_set_ph(void *h, int i, const float *stats, float margin, long last, long mode);
 
 static int all_finite(const double *v, int n)
 {
@@ -242,6 +243,17 @@ void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, l
     if (margin) *margin = o->ph_margin[i];
     if (last) *last = o->ph_last[i];
     if (mode) *mode = o->mode[i];
+}
+
+/* Overwrite instance i's Page-Hinkley state and mode (the parity harness
+ * adopts the GPU's when an alarm comparison sat within rounding of lambda). */
+void ora_set_ph(void *h, int i, const float *stats, float margin, long last, long mode)
+{
+    ora_t *o = (ora_t *)h;
+    memcpy(o->ph + (size_t)i * 6, stats, sizeof(float) * 6);
+    o->ph_margin[i] = margin;
+    o->ph_last[i] = last;
+    o->mode[i] = mode;
 }
 
 /* Parameters of pruning rules 2-8 (see the header). */

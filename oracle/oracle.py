@@ -35,6 +35,7 @@ def _declare(lib):
     lib.ora_get_rsum.argtypes = [P, I, P]
     lib.ora_set_exploit.argtypes = [P, I, D, D, I, I]
     lib.ora_get_ph.argtypes = [P, I, P, P, P, P]
+    lib.ora_set_ph.argtypes = [P, I, P, ctypes.c_float, L, L]
     lib.ora_commit.argtypes = [P, P, P, P]
     lib.ora_flush.argtypes = [P, P]
     lib.ora_get.argtypes = [P, I, P, P, P, P, P, P, P]
@@ -99,6 +100,11 @@ class Oracle:
         self.lib.ora_get_ph(self.h, int(i), _ptr(stats), ctypes.byref(margin), ctypes.byref(last),
                             ctypes.byref(mode))
         return stats, margin.value, last.value, mode.value
+
+    def set_page_hinkley(self, i, stats, margin, last, mode):
+        """Overwrite instance i's Page-Hinkley state and mode."""
+        st = np.ascontiguousarray(stats, dtype=np.float32)
+        self.lib.ora_set_ph(self.h, int(i), _ptr(st), float(margin), int(last), int(mode))
 
     def set_heuristics(self, ext_rounds, ext_min_n, ext_thr, hist_after, hist_min_n, hist_kappa,
                        hist_min_arms, cascade_k):

@@ -9,7 +9,7 @@ from .oracle import Oracle
 
 
 def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, lib=None,
-                    margins=False):
+                    margins=False, on_create=None):
     """Run T decisions of len(instances) tuners against the fp64 environment.
 
     arrivals, noise: [T+1][n] exogenous draws (agft_workloads.exogenous).
@@ -19,12 +19,14 @@ def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, l
     of the pruning-rule comparisons from their thresholds.
     Returns a dict with the oracle object, actions [T][n] and, if record is
     set, contexts [T][n][d], rewards [T][n] (reward of decision t) and
-    ucb/lcb [T][n][K].
+    ucb/lcb [T][n][K].  on_create(oracle) is called once the oracle exists.
     """
     T = wl.T if T is None else int(T)
     env = Env(wl, arrivals, noise, T)
     n = env.n
     ora = Oracle.from_workload(wl, B=n, lib=lib)
+    if on_create is not None:
+        on_create(ora)
     x = env.reset()
     r_prev = None
     actions = np.empty((T, n), dtype=np.int32)

@@ -27,7 +27,9 @@ class agft_config(ctypes.Structure):
                 ("flags", _u32),
                 ("ext_rounds", _i32), ("ext_min_n", _i32), ("ext_thr", _f32),
                 ("hist_after", _i32), ("hist_min_n", _i32), ("hist_kappa", _f32),
-                ("hist_min_arms", _i32), ("cascade_k", _i32)]
+                ("hist_min_arms", _i32), ("cascade_k", _i32),
+                ("exploit", _i32), ("ph_delta", _f32), ("ph_lambda", _f32),
+                ("ph_window", _i32), ("ph_min_rounds", _i32)]
 
 
 class agft_state_view(ctypes.Structure):
@@ -45,6 +47,8 @@ class agft_env_config(ctypes.Structure):
                 ("q_cap", _i32), ("run_cap", _i32),
                 ("mu", _f32 * 7), ("sd", _f32 * 7)]
 
+
+ABI_VERSION = 2   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
             "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version",
@@ -97,7 +101,11 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_2508_01744_amd._build` (hipcc, gfx950)")
-        _lib = _declare(ctypes.CDLL(LIB_PATH))
+        handle = _declare(ctypes.CDLL(LIB_PATH))
+        if handle.agft_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {handle.agft_abi_version()}, these "
+                               f"bindings expect {ABI_VERSION}: rebuild it")
+        _lib = handle
     return _lib
 
 

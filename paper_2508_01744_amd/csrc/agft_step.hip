@@ -105,9 +105,12 @@ __device__ inline void unpack(int e, int &i, int &j) {
 }
 
 // Per-instance block of 32-bit words: previous action, active-arm count,
-// non-finite-input count, a spare word, then the stashed context.  Kept
+// non-finite-input count, mode (-1 exploring, else the round exploitation
+// began), the Page-Hinkley state (n, mean, m+, min m+, m-, min m-), the round
+// of its last alarm, its last margin, then the stashed context.  Kept
 // together so the epilogue writes one or two lines per instance.
-constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstX = 4;
+constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstMode = 3, kInstPh = 4,
+              kInstPhLast = 10, kInstPhMargin = 11, kInstX = 12;
 
 int inst_words(int d) { return (kInstX + d + 15) / 16 * 16; }
 
@@ -170,12 +173,21 @@ struct Heuristics {
     int32_t hist_min_arms, cascade_k;
 };
 
+// Switch to greedy exploitation after a Page-Hinkley test finds the
+// reward sequence stable (Sec. 4.2, Eq. 2).
+struct Exploit {
+    int32_t on;
+    float delta, lambda;
+    int32_t window, min_rounds;
+};
+
 struct StepArgs {
     float4 *arms;
     uint32_t *mask;
     int32_t *inst;        // [B][IW] per-instance blocks
     int2 *stats;          // [B][K] rewards folded in, their sum (fp32 bits)
     Heuristics h;
+    Exploit e;
     int64_t t;            // decisions made before this step
     StateHeader *hdr;
     const float *ctx;     // [B][D] or nullptr (flush)
@@ -299,6 +311,46 @@ void agft_step_kernel(StepArgs p) {
 #pragma unroll
         for (int q = 0; q < D; ++q) xp[q] = xpi[q];
     }
+
+    // Page-Hinkley test on the instance's rewards and the switch to greedy
+    // exploitation (uniform scalar code, single precision, fixed order).
+    int mode = p.e.on ? blk[kInstMode] : -1;
+    float ph[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int ph_last = 0;
+    float ph_margin = 0.0f;
+    if (p.e.on) {
+#pragma unroll
+        for (int q = 0; q < 6; ++q) ph[q] = __int_as_float(blk[kInstPh + q]);
+        ph_last = blk[kInstPhLast];
+        ph_margin = __int_as_float(blk[kInstPhMargin]);
+        if (upd && mode < 0) {
+            ph[0] = ph[0] + 1.0f;
+            ph[1] = ph[1] + (r - ph[1]) / ph[0];
+            ph[2] = ph[2] + ((r - ph[1]) - p.e.delta);
+            ph[3] = fminf(ph[3], ph[2]);
+            ph[4] = ph[4] + ((ph[1] - r) - p.e.delta);
+            ph[5] = fminf(ph[5], ph[4]);
+            const float up = ph[2] - ph[3], dn = ph[4] - ph[5];
+            ph_margin = p.e.lambda - (up > dn ? up : dn);
+            if (up > p.e.lambda || dn > p.e.lambda) {
+                ph_last = (int)p.t;
+#pragma unroll
+                for (int q = 0; q < 6; ++q) ph[q] = 0.0f;
+            }
+        }
+        if (mode < 0 && x_ok && p.t >= p.e.min_rounds && p.t - ph_last >= p.e.window) mode = (int)p.t;
+    }
+    const bool greedy = mode >= 0;
+    // The block's words 3..11 after this step, parked in LDS by the lanes that
+    // store them at the end (so they hold no registers through the stream; every
+    // wave has read the old words before any lane writes the new ones).
+    __shared__ int s_phw[kInstX - kInstMode];
+    const bool ph_lane = p.e.on && tid >= kInstMode && tid < kInstX;
+    if (ph_lane)
+        s_phw[tid - kInstMode] = tid == kInstMode ? mode
+                               : tid == kInstPhLast ? ph_last
+                               : tid == kInstPhMargin ? __float_as_int(ph_margin)
+                               : __float_as_int(pick<6>(ph, tid - kInstPh));
 
     // Record of the previous decision's arm: fetched now, consumed after the stream.
     float4 old_chunk[NQ];
@@ -458,7 +510,25 @@ void agft_step_kernel(StepArgs p) {
 
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
     const int nlist = s_nlist;
-    {
+    if (greedy) {
+        // Eq. 2: only theta_k^T x_t, from the one chunk of each lane slice that
+        // holds its two theta entries (positions d+1, d+2)
+        constexpr int TC = D / 4;
+        for (int base = 0; base < nlist; base += apw) {
+            const int slot = base + grp;
+            const int k_cur = slot < nlist ? s_list[slot] : -1;
+            float m = 0.0f;
+            if (k_cur >= 0) {
+                const float4 v = ld_nt(recs + (size_t)k_cur * R::R + TC * G + j);
+                m = fmaf(v.z, xt1, v.y * xt0);
+            }
+            m = group_sum<G>(m);
+            if (k_cur >= 0 && j == 0) {
+                s_ucb[k_cur] = m;
+                s_lcb[k_cur] = m;
+            }
+        }
+    } else {
         float4 cur[S], nxt[S];
         int k_cur = grp < nlist ? s_list[grp] : -1;
         if (k_cur >= 0) {
@@ -593,8 +663,8 @@ void agft_step_kernel(StepArgs p) {
             w2 = group_sum<G>(w2);
             if (lane == 0) {
                 const float w = sqrtf(w2);
-                s_ucb[a_upd] = fmaf(p.alpha, w, m);
-                s_lcb[a_upd] = fmaf(-p.alpha, w, m);
+                s_ucb[a_upd] = greedy ? m : fmaf(p.alpha, w, m);
+                s_lcb[a_upd] = greedy ? m : fmaf(-p.alpha, w, m);
             }
         }
     } else if (has_prev && tid == 0) {
@@ -606,6 +676,7 @@ void agft_step_kernel(StepArgs p) {
             blk[kInstAprev] = -1;
             if (inst == 0) p.hdr->pending = 0;
         }
+        if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
         return;
     }
 
@@ -626,6 +697,7 @@ void agft_step_kernel(StepArgs p) {
                 p.hdr->pending = 1;
             }
         }
+        if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
         return;
     }
     __syncthreads();
@@ -633,7 +705,8 @@ void agft_step_kernel(StepArgs p) {
     // ---- pruning and argmax over the scores in LDS ----
     auto is_active = [&](int k) { return k < K && ((s_mask[k >> 5] >> (k & 31)) & 1u) != 0; };
     float lstar = -INFINITY;
-    if (p.prune_now) {
+    const bool prune_now = p.prune_now && !greedy;
+    if (prune_now) {
         float l = -INFINITY;
         for (int k = tid; k < K; k += nthr)
             if (is_active(k)) l = fmaxf(l, s_lcb[k]);
@@ -659,7 +732,7 @@ void agft_step_kernel(StepArgs p) {
             sc[k] = u;
             sc[K + k] = act ? s_lcb[k] : -INFINITY;
         }
-        if (p.prune_now) {
+        if (prune_now) {
             const unsigned long long bal = __ballot(keep);
             const int w0 = (base + wave * kWave) >> 5;
             uint32_t *mwo = p.mask + (size_t)inst * KW;
@@ -697,6 +770,7 @@ void agft_step_kernel(StepArgs p) {
         }
         if (lane == kInstAprev) blk[kInstAprev] = a;
         if (lane == kInstKact) blk[kInstKact] = cnt;
+        if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
         if (lane >= kInstX && lane < kInstX + D)
             reinterpret_cast<float *>(blk)[lane] = pick<D>(x, lane - kInstX);
     }
@@ -744,7 +818,10 @@ __global__ void agft_init_kernel(InitArgs p) {
     for (size_t idx = gtid; idx < (size_t)p.B * p.K; idx += gsz) p.stats[idx] = make_int2(0, 0);
     for (size_t idx = gtid; idx < (size_t)p.B * p.IW; idx += gsz) {
         const int w = (int)(idx % p.IW);
-        p.inst[idx] = w == kInstAprev ? -1 : (w == kInstKact ? p.K : 0);
+        p.inst[idx] = w == kInstAprev || w == kInstMode ? -1
+                    : w == kInstKact ? p.K
+                    : w == kInstPhMargin ? 0x7f800000   // +inf: no test yet
+                    : 0;
     }
     if (gtid == 0) *p.hdr = p.h;
 }
@@ -806,6 +883,10 @@ bool config_ok(const agft_config *c) {
                                 !std::isfinite(c->hist_kappa) || c->hist_kappa < 0.0f))
         return false;
     if ((c->prune_rule & 8) && (c->cascade_k < 0 || c->cascade_k > c->K)) return false;
+    if (c->exploit != 0 && c->exploit != 1) return false;
+    if (c->exploit && (!std::isfinite(c->ph_delta) || !std::isfinite(c->ph_lambda) || c->ph_lambda < 0.0f ||
+                       c->ph_window < 0 || c->ph_min_rounds < 0))
+        return false;
     if ((c->flags & ~AGFT_ADOPT_STATE) != 0) return false;
     return true;
 }
@@ -931,6 +1012,11 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.h.hist_min_arms = c.hist_min_arms;
     p.h.cascade_k = c.cascade_k;
     p.t = h->t;
+    p.e.on = c.exploit;
+    p.e.delta = c.ph_delta;
+    p.e.lambda = c.ph_lambda;
+    p.e.window = c.ph_window;
+    p.e.min_rounds = c.ph_min_rounds;
     p.hdr = at<StateHeader>(h->base, 0);
     p.ctx = d_ctx;
     p.reward = d_reward;

@@ -20,7 +20,7 @@ class Tuner:
 
     def __init__(self, B, K, d, lam=1.0, alpha0=1.0, alpha_sched=0, prune_rule=0,
                  prune_period=50, device="cuda", stream=None, state=None, adopt=False,
-                 heuristics=None):
+                 heuristics=None, exploit=None):
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
@@ -29,6 +29,10 @@ class Tuner:
                                  L.AGFT_ADOPT_STATE if adopt else 0)
         for name, value in (heuristics or {}).items():
             setattr(self.cfg, name, value)
+        if exploit:
+            self.cfg.exploit = 1
+            for name, value in exploit.items():
+                setattr(self.cfg, name, value)
         self.nbytes = L.agft_state_bytes(self.cfg)
         if self.nbytes == 0:
             raise ValueError("invalid tuner configuration")
@@ -51,7 +55,8 @@ class Tuner:
     @classmethod
     def from_workload(cls, wl, B=None, **kw):
         return cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0, wl.alpha_sched,
-                   wl.prune, wl.period, heuristics=wl.heuristics(), **kw)
+                   wl.prune, wl.period, heuristics=wl.heuristics(),
+                   exploit=wl.page_hinkley() if wl.exploit else None, **kw)
 
     def close(self):
         if getattr(self, "h", None):
@@ -115,8 +120,8 @@ class Tuner:
             arms=region(v.arms, B * K * C * 4, torch.float32, (B, K, C, 4)),
             mask=region(v.mask, B * KW, torch.int32, (B, KW)),
             inst=inst,
-            aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2],
-            xprev=inst[:, 4:4 + d].view(torch.float32),
+            aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2], mode=inst[:, 3], ph=inst[:, 3:12],
+            xprev=inst[:, 12:12 + d].view(torch.float32),
             stats=region(v.stats, B * K * 2, torch.int32, (B, K, 2)),
         )
 

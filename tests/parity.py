@@ -11,6 +11,14 @@ Closed loop (compare): the oracle also runs its own fp64 environment on the
 same exogenous draws, so GPU contexts and rewards are checked too.
 Open loop (compare_open_loop): both sides get the same given contexts and
 rewards.
+
+The Page-Hinkley test behind the switch to exploitation runs in single
+precision on both sides in the same order.  In the open loop its state must
+match bit for bit.  In the closed loop the rewards differ by rounding, so its
+state is compared within PH_TOL, and an alarm that one side raised and the
+other did not is accepted only where the oracle's margin was within PH_TIE of
+zero; the oracle then adopts the GPU's test state (and, for that step, the
+GPU's decision, since the two scored in different modes).
 """
 import numpy as np
 
@@ -20,6 +28,8 @@ from oracle import Oracle, run_closed_loop
 SCORE_TOL = 1e-4   # |s_gpu - s_oracle| <= SCORE_TOL * max(1, |s_oracle|)
 TIE = 1e-5         # score gaps at or below this (times max(1, |score|)) are near-ties
 ENV_TOL = 1e-5     # contexts and rewards: fp32 environment vs fp64 environment
+PH_TOL = 1e-4      # Page-Hinkley statistics, closed loop (both fp32, rewards differ by rounding)
+PH_TIE = 1e-4      # |lambda - statistic| at or below this: the alarm could go either way
 
 
 def mask_words_to_bool(words, K):
@@ -34,13 +44,54 @@ class ParityError(AssertionError):
 
 class Checker:
     def __init__(self, name, K, ids, g_a, g_keep, g_s=None, g_x=None, g_r=None, rules=0,
-                 cascade_k=0):
+                 cascade_k=0, g_ph=None, strict_ph=False):
         self.name, self.K, self.ids = name, K, list(ids)
         self.g_a, self.g_keep, self.g_s, self.g_x, self.g_r = g_a, g_keep, g_s, g_x, g_r
         self.rules, self.cascade_k = rules, cascade_k
+        # g_ph [T][n][9] int32: mode, Page-Hinkley n, mean, m+, min m+, m-, min m-,
+        # last alarm round, last margin (fp32 bits), after each step
+        self.g_ph, self.strict_ph = g_ph, strict_ph
+        self.oracle = None
         self.st = dict(max_score_err=0.0, max_ctx_err=0.0, max_reward_err=0.0, forced=0,
                        forced_prune=0, forced_rules=0, exact_tie_steps=0, decisions=0,
-                       no_decision=0)
+                       no_decision=0, max_ph_err=0.0, forced_ph=0, forced_mode=0,
+                       greedy_decisions=0)
+
+    def bind(self, oracle):
+        """The oracle whose Page-Hinkley state is checked (and forced)."""
+        self.oracle = oracle
+
+    def _check_ph(self, t, i):
+        """Compare instance i's test state after step t; returns True when the
+        two sides scored this step in different modes (decision forced)."""
+        g = np.asarray(self.g_ph[t, i], dtype=np.int32)
+        g_mode, g_last = int(g[0]), int(g[7])
+        g_stats = g[1:7].view(np.float32)
+        g_margin = float(g[8:9].view(np.float32)[0])
+        o_stats, o_margin, o_last, o_mode = self.oracle.page_hinkley(i)
+        if g_mode == o_mode and g_last == o_last:
+            if self.strict_ph:
+                if not (np.array_equal(g_stats.view(np.int32), o_stats.view(np.int32))
+                        and np.float32(g_margin) == np.float32(o_margin)):
+                    self.fail(f"Page-Hinkley state differs at t={t}, instance {self.ids[i]}: "
+                              f"{g_stats} {g_margin} vs {o_stats} {o_margin}")
+            else:
+                err = np.abs(g_stats.astype(np.float64) - o_stats) / np.maximum(1.0, np.abs(o_stats))
+                self.st["max_ph_err"] = max(self.st["max_ph_err"], float(err.max()))
+                if err.max() > PH_TOL:
+                    self.fail(f"Page-Hinkley statistics differ at t={t}, instance {self.ids[i]}: "
+                              f"{g_stats} vs {o_stats}")
+            return False
+        if self.strict_ph or g_last == o_last or abs(o_margin) > PH_TIE:
+            self.fail(f"Page-Hinkley test differs at t={t}, instance {self.ids[i]}: GPU mode {g_mode}, "
+                      f"last alarm {g_last}; oracle mode {o_mode}, last alarm {o_last}, "
+                      f"margin {o_margin}")
+        self.oracle.set_page_hinkley(i, g_stats, g_margin, g_last, g_mode)
+        self.st["forced_ph"] += 1
+        if (g_mode >= 0) != (o_mode >= 0):
+            self.st["forced_mode"] += 1
+            return True
+        return False
 
     def fail(self, msg):
         raise ParityError(f"{self.name}: {msg}")
@@ -77,6 +128,13 @@ class Checker:
         commit_a = action.copy()
         for i in range(len(ids)):
             ga = int(self.g_a[t, i])
+            if self.g_ph is not None:
+                if self._check_ph(t, i):
+                    commit_keep[i] = self.g_keep[t, i]
+                    commit_a[i] = ga
+                    continue
+                if self.g_ph[t, i, 0] >= 0 and action[i] >= 0:
+                    st["greedy_decisions"] += 1
             if self.g_s is not None:
                 g_act = np.isfinite(self.g_s[t, i, 0])
                 if not np.array_equal(g_act, act[i]):
@@ -145,26 +203,34 @@ def compare(wl, T, probes, rec):
                   mask_words_to_bool(rec["mask"].numpy(), wl.K),
                   rec["scores"].numpy().astype(np.float64) if "scores" in rec else None,
                   rec["x"].numpy().astype(np.float64), rec["r"].numpy().astype(np.float64),
-                  rules=wl.prune, cascade_k=wl.cascade_k)
-    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14))
+                  rules=wl.prune, cascade_k=wl.cascade_k,
+                  g_ph=rec["ph"].numpy() if wl.exploit else None)
+    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14),
+                          on_create=chk.bind)
     st = chk.finish()
     st["oracle"] = out["oracle"]
     return st
 
 
-def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s):
+def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None):
     """Open loop: contexts X [T][B][d] and rewards R [T][B] (reward of the
     decision at t) given to both sides.  cfg: dict(B, K, d, lam, alpha0,
-    sched, prune, period).  GPU records: actions [T][B], mask words
-    [T][B][KW] after each step, scores [T][B][2][K]."""
+    sched, prune, period[, heuristics][, exploit]).  GPU records: actions
+    [T][B], mask words [T][B][KW] after each step, scores [T][B][2][K],
+    Page-Hinkley words [T][B][9] (when cfg has exploit)."""
     T = X.shape[0]
     ora = Oracle(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
                  cfg["prune"], cfg["period"])
     heur = cfg.get("heuristics")
     if heur:
         ora.set_heuristics(**heur)
+    expl = cfg.get("exploit")
+    if expl:
+        ora.set_exploit(True, **expl)
     chk = Checker(name, cfg["K"], range(cfg["B"]), g_a, mask_words_to_bool(g_masks, cfg["K"]), g_s,
-                  rules=cfg["prune"], cascade_k=(heur or {}).get("cascade_k", 0))
+                  rules=cfg["prune"], cascade_k=(heur or {}).get("cascade_k", 0),
+                  g_ph=g_ph if expl else None, strict_ph=True)
+    chk.bind(ora)
     r_prev = None
     for t in range(T):
         ucb, lcb, keep, action, marg = ora.decide(X[t], r_prev, margins=True)

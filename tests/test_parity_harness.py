@@ -1,0 +1,81 @@
+"""The parity harness itself, on the CPU: a record made by the oracle passes
+the open-loop comparison, and a record with one planted difference fails it.
+(The record here is the oracle's own, so these tests say nothing about the
+GPU; they check that the comparison would catch what it is meant to.)"""
+import numpy as np
+import pytest
+
+import parity
+from oracle import Oracle
+
+FAST_PH = dict(ph_delta=0.05, ph_lambda=5.0, ph_window=40, ph_min_rounds=60)
+
+
+def _inputs(seed, T, B, d):
+    rng = np.random.default_rng(seed)
+    X = rng.standard_normal((T, B, d))
+    X[:, :, 0] = 1.0
+    R = rng.uniform(-2.0, 0.0, size=(T, B))
+    R[T // 2:, ::2] -= 1.5
+    return X.astype(np.float32).astype(np.float64), R.astype(np.float32).astype(np.float64)
+
+
+def _record(cfg, X, R):
+    """Run the oracle and keep what the GPU run records, in the GPU's formats."""
+    T, B, _ = X.shape
+    K = cfg["K"]
+    ora = Oracle(B, K, cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"], cfg["prune"], cfg["period"])
+    ora.set_exploit(True, **cfg["exploit"])
+    KW = (K + 31) // 32
+    acts = np.empty((T, B), np.int32)
+    masks = np.zeros((T, B, KW), np.int64)
+    scores = np.empty((T, B, 2, K))
+    ph = np.empty((T, B, 9), np.int32)
+    r_prev = None
+    for t in range(T):
+        ucb, lcb, keep, action = ora.decide(X[t], r_prev)
+        ora.commit(X[t], action, keep)
+        acts[t] = action
+        for k in range(K):
+            masks[t, :, k // 32] |= keep[:, k].astype(np.int64) << (k % 32)
+        scores[t, :, 0], scores[t, :, 1] = ucb, lcb
+        for i in range(B):
+            st, margin, last, mode = ora.page_hinkley(i)
+            ph[t, i, 0] = mode
+            ph[t, i, 1:7] = st.view(np.int32)
+            ph[t, i, 7] = last
+            ph[t, i, 8] = np.float32(margin).view(np.int32)
+        r_prev = R[t]
+    return acts, masks.astype(np.uint32).view(np.int32), scores.astype(np.float32).astype(np.float64), ph
+
+
+CFG = dict(B=6, K=12, d=8, lam=1.0, alpha0=0.5, sched=0, prune=1, period=20, exploit=FAST_PH)
+
+
+def test_oracle_record_passes():
+    X, R = _inputs(3, 150, CFG["B"], CFG["d"])
+    a, m, s, ph = _record(CFG, X, R)
+    assert (ph[-1, :, 0] >= 0).any() and (ph[:, :, 7] > 0).any()
+    st = parity.compare_open_loop("self", CFG, X, R, a, m, s, g_ph=ph)
+    assert st["greedy_decisions"] > 0 and st["forced_ph"] == 0
+
+
+@pytest.mark.parametrize("plant", ["switch_round", "alarm_round", "statistic", "greedy_score"])
+def test_planted_difference_fails(plant):
+    X, R = _inputs(3, 150, CFG["B"], CFG["d"])
+    a, m, s, ph = _record(CFG, X, R)
+    modes = ph[-1, :, 0]
+    i = int(np.flatnonzero(modes >= 0)[0])
+    t_sw = int(modes[i])
+    if plant == "switch_round":         # the record switches one step late
+        ph[t_sw, i, 0] = -1
+    elif plant == "alarm_round":        # an alarm one round off
+        t = int(np.flatnonzero(ph[:, :, 7].max(axis=1) > 0)[0])
+        j = int(np.flatnonzero(ph[t, :, 7] > 0)[0])
+        ph[t:, j, 7] += 1
+    elif plant == "statistic":          # one ulp in the running mean
+        ph[t_sw // 2, i, 2] += 1
+    else:                               # a greedy score off by 1e-3
+        s[t_sw + 1, i, :, int(a[t_sw + 1, i])] += 1e-3
+    with pytest.raises(parity.ParityError):
+        parity.compare_open_loop("planted", CFG, X, R, a, m, s, g_ph=ph)
