@@ -36,20 +36,30 @@ def record_floats(d):
     return d + d * (d + 1) // 2
 
 
-def step_bytes(wl, kact_total, prune_step, update):
+def step_bytes(wl, scored_exploring, scored_greedy, mask_write, update):
     """Algorithmic HBM bytes of one step kernel launch.
 
-    Per instance: the active arms' records are read once (the previous
-    decision's arm in the update phase, the others in the scoring phase), the
-    updated record is written once; plus context, stashed context, reward,
-    action, bookkeeping words and the action-set mask (written at pruning
-    steps).  kact_before: active arms per instance when the step starts.
+    Per instance: the previous decision's arm is read and written back once
+    (its model: the d(d+1)/2 factor entries and theta, with its reward count
+    and sum); every other arm scored is read once, as its whole model while
+    the instance explores (Eq. 1) and as theta alone once it exploits (Eq. 2);
+    plus context, stashed context, reward, action and bookkeeping words, the
+    per-arm reward statistics when the paper's rules 2-8 are on, the
+    Page-Hinkley words when the switch is on, and the action-set mask (written
+    back when a rule may remove arms).  scored_*: arms scored, the previous
+    decision's arm excluded, summed over the instances in each mode.
     """
-    s = record_floats(wl.d)
+    B, d = wl.B, wl.d
+    s = record_floats(d)
     kw = (wl.K + 31) // 32
-    records = 4 * s * (kact_total + (wl.B if update else 0))
-    io = wl.B * 4 * (3 * wl.d + 7)     # ctx, xprev r/w; reward, action, aprev r/w, kact, nsel r/w
-    mask = wl.B * 4 * kw * (2 if prune_step else 1)
+    upd = B if update else 0
+    records = 4 * s * (scored_exploring + 2 * upd) + 4 * d * scored_greedy + 16 * upd
+    io = B * 4 * (3 * d + 7)           # ctx, xprev r/w; reward, action, aprev r/w, kact, bad
+    if wl.prune & 14:
+        io += B * 8 * wl.K             # per-arm count and reward sum
+    if wl.exploit:
+        io += B * 4 * 9 * 2            # mode and test state r/w
+    mask = B * 4 * kw * (2 if mask_write else 1)
     return float(records + io + mask)
 
 
@@ -125,17 +135,32 @@ def main():
         tuner.close()
         tuner = Tuner.from_workload(wl, device=dev, state=state)
 
-    def run(nsteps, kernel_events=None, kact_log=None):
+    def run(nsteps, kernel_events=None, scored_log=None):
         x = env.reset()
         r = None
+        if scored_log is not None:
+            sc = torch.empty(wl.B, 2, wl.K, device=dev)
+            rows = torch.arange(wl.B, device=dev)
+            prev = torch.empty_like(action)
+            view = tuner.view()
         for t in range(nsteps):
-            if kact_log is not None:
-                kact_log.append(tuner.view()["kact"].sum())
             if kernel_events is not None:
                 kernel_events[t][0].record(stream)
-            tuner.step(x, r, action)
+            tuner.step(x, r, action, sc if scored_log is not None else None)
             if kernel_events is not None:
                 kernel_events[t][1].record(stream)
+            if scored_log is not None:
+                # arms scored this step, the one updated from the previous decision excluded,
+                # split by the instance's mode (the mode word after the step)
+                fin = torch.isfinite(sc[:, 0, :])
+                if t > 0:
+                    ok = prev >= 0
+                    fin[rows[ok], prev[ok].long()] = False
+                n = fin.sum(dim=1)
+                greedy = view["mode"] >= 0
+                scored_log.append(torch.stack([(n * ~greedy).sum(), (n * greedy).sum(),
+                                               view["kact"].sum(), greedy.sum()]))
+                prev.copy_(action)
             r, x = env.step(t, action)
 
     # warm-up on a fresh state, then re-initialise
@@ -157,11 +182,11 @@ def main():
     elapsed_ms = start.elapsed_time(stop)
     kernel_ms = np.array([a.elapsed_time(b) for a, b in ev])
 
-    # the run is deterministic: replay it untimed to log the active-arm counts
+    # the run is deterministic: replay it untimed to log the arms each step scored
     fresh()
-    kact_log = []
-    run(K, kact_log=kact_log)
-    kact_before = [int(v) for v in torch.stack(kact_log).cpu()] if kact_log else []
+    scored_log = []
+    run(K, scored_log=scored_log)
+    scored = torch.stack(scored_log).cpu().numpy().astype(np.int64) if scored_log else np.zeros((0, 4))
     torch.cuda.synchronize()
 
     if args.calibrate_copy:
@@ -174,8 +199,8 @@ def main():
 
     total_bytes = 0.0
     for t in range(K):
-        prune_step = wl.prune == 1 and t > 0 and t % wl.period == 0
-        total_bytes += step_bytes(wl, kact_before[t], prune_step, update=t > 0)
+        mask_write = bool(wl.prune & 14) or (wl.prune & 1 and t > 0 and t % wl.period == 0)
+        total_bytes += step_bytes(wl, int(scored[t, 0]), int(scored[t, 1]), mask_write, update=t > 0)
     bytes_per_launch = total_bytes / K
     kernel_avg_ms = float(kernel_ms.mean())
     achieved = bytes_per_launch / (kernel_avg_ms * 1e-3) / 1e9
@@ -208,7 +233,9 @@ def main():
         "detail": {"step_kernel_avg_ms": kernel_avg_ms,
                    "step_kernel_share": float(kernel_ms.sum() / elapsed_ms),
                    "algorithmic_bytes_per_launch": bytes_per_launch,
-                   "mean_active_arms": float(np.mean(kact_before) / wl.B) if kact_before else None,
+                   "mean_scored_arms": float(scored[:, :2].sum(axis=1).mean() / wl.B) if K else None,
+                   "mean_active_arms_after_step": float(scored[:, 2].mean() / wl.B) if K else None,
+                   "exploiting_fraction": float(scored[:, 3].mean() / wl.B) if K else None,
                    "wall_s": t_wall},
     }
     if not args.no_cpu_baseline:

@@ -99,7 +99,10 @@ typedef struct agft_config {
        test restarts).  Once t >= ph_min_rounds and no alarm came in the last
        ph_window rounds, the instance exploits for good: a_t = argmax over the
        active arms of theta_k^T x_t (reported as both UCB and LCB), reading only
-       the theta chunk of each record; rule 1 is not applied; updates go on. */
+       the contiguous copy of theta that the state holds when this is on (4*d
+       bytes per arm, against 2*d*(d+4) for a whole record); rule 1 is not
+       applied; updates go on.  A buffer adopted with AGFT_ADOPT_STATE must have
+       been made with the same setting. */
     int32_t exploit;
     float ph_delta;        /* finite */
     float ph_lambda;       /* finite, >= 0 */
@@ -136,11 +139,15 @@ typedef struct agft_state_view {
     int32_t inst_words; /* words per instance block: 12 + d rounded up to 16 */
     int32_t *stats;     /* [B][K][2] per arm: [0] rewards folded in (int32),
                            [1] their sum (fp32 bits) */
+    float *theta;       /* [B][K][d] copy of theta_k (Eq. 5), kept in step with the
+                           records, which exploiting instances read in their place;
+                           NULL when cfg.exploit is 0 */
 } agft_state_view;
 
 /* Bytes of device state for cfg (a 256-byte header, then the arm records,
- * the masks, the instance blocks and the arm statistics of agft_state_view,
- * each region 256-byte aligned); 0 if cfg is invalid. */
+ * the masks, the instance blocks, the arm statistics and, with cfg.exploit,
+ * the theta copy of agft_state_view, each region 256-byte aligned); 0 if cfg
+ * is invalid. */
 size_t agft_state_bytes(const agft_config *cfg);
 
 /*

@@ -35,7 +35,7 @@ class agft_config(ctypes.Structure):
 class agft_state_view(ctypes.Structure):
     _fields_ = [("t", _i64), ("pending", _i32), ("B", _i32), ("K", _i32), ("d", _i32),
                 ("chunks", _i32), ("mask_words", _i32), ("arms", _vp), ("mask", _vp),
-                ("inst", _vp), ("inst_words", _i32), ("stats", _vp)]
+                ("inst", _vp), ("inst_words", _i32), ("stats", _vp), ("theta", _vp)]
 
 
 class agft_env_config(ctypes.Structure):

@@ -63,7 +63,8 @@ struct alignas(16) StateHeader {
     int64_t t;
     float lambda, alpha0;
     int32_t alpha_sched, prune_rule, prune_period;
-    uint32_t reserved[47];
+    int32_t exploit;      // 1: the buffer holds the theta copy of the switch
+    uint32_t reserved[46];
 };
 static_assert(sizeof(StateHeader) == 256, "header is 256 bytes");
 
@@ -115,10 +116,11 @@ constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstMode = 3, kInstP
 int inst_words(int d) { return (kInstX + d + 15) / 16 * 16; }
 
 struct Layout {
-    size_t arms, mask, inst, stats, total;
+    size_t arms, mask, inst, stats, theta, total;
 };
 
-Layout layout_for(int B, int K, int d) {
+// theta copy [B][K][d] only with the switch to exploitation (0 bytes otherwise)
+Layout layout_for(int B, int K, int d, int exploit) {
     Layout L;
     const size_t b = (size_t)B, k = (size_t)K;
     const size_t kw = (k + 31) / 32;
@@ -127,6 +129,7 @@ Layout layout_for(int B, int K, int d) {
     L.mask = off;  off = align_up(off + b * kw * 4);
     L.inst = off;  off = align_up(off + b * (size_t)inst_words(d) * 4);
     L.stats = off; off = align_up(off + b * k * 8);
+    L.theta = off; off = align_up(off + (exploit ? b * k * (size_t)d * 4 : 0));
     L.total = off;
     return L;
 }
@@ -186,6 +189,7 @@ struct StepArgs {
     uint32_t *mask;
     int32_t *inst;        // [B][IW] per-instance blocks
     int2 *stats;          // [B][K] rewards folded in, their sum (fp32 bits)
+    float *theta;         // [B][K][D] copy of theta (exploitation on), else nullptr
     Heuristics h;
     Exploit e;
     int64_t t;            // decisions made before this step
@@ -511,19 +515,23 @@ void agft_step_kernel(StepArgs p) {
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
     const int nlist = s_nlist;
     if (greedy) {
-        // Eq. 2: only theta_k^T x_t, from the one chunk of each lane slice that
-        // holds its two theta entries (positions d+1, d+2)
-        constexpr int TC = D / 4;
-        for (int base = 0; base < nlist; base += apw) {
-            const int slot = base + grp;
+        // Eq. 2: only theta_k^T x_t, read from the contiguous theta copy by
+        // groups of D/4 lanes (one float4 each)
+        constexpr int GT = D / 4;
+        const int jt = tid % GT, gt = tid / GT, apt = nthr / GT;
+        const float x0 = pick<D>(x, 4 * jt), x1 = pick<D>(x, 4 * jt + 1);
+        const float x2 = pick<D>(x, 4 * jt + 2), x3 = pick<D>(x, 4 * jt + 3);
+        const float4 *th = reinterpret_cast<const float4 *>(p.theta + (size_t)inst * K * D);
+        for (int base = 0; base < nlist; base += apt) {
+            const int slot = base + gt;
             const int k_cur = slot < nlist ? s_list[slot] : -1;
             float m = 0.0f;
             if (k_cur >= 0) {
-                const float4 v = ld_nt(recs + (size_t)k_cur * R::R + TC * G + j);
-                m = fmaf(v.z, xt1, v.y * xt0);
+                const float4 v = ld_nt(th + (size_t)k_cur * GT + jt);
+                m = fmaf(v.w, x3, fmaf(v.z, x2, fmaf(v.y, x1, v.x * x0)));
             }
-            m = group_sum<G>(m);
-            if (k_cur >= 0 && j == 0) {
+            m = group_sum<GT>(m);
+            if (k_cur >= 0 && jt == 0) {
                 s_ucb[k_cur] = m;
                 s_lcb[k_cur] = m;
             }
@@ -643,6 +651,10 @@ void agft_step_kernel(StepArgs p) {
                 v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
             }
             dst[c] = make_float4(v[0], v[1], v[2], v[3]);
+        }
+        if (p.theta != nullptr && tid < D / 4) {
+            float4 *tdst = reinterpret_cast<float4 *>(p.theta + ((size_t)inst * K + a_upd) * D);
+            tdst[tid] = make_float4(s_new[4 * tid], s_new[4 * tid + 1], s_new[4 * tid + 2], s_new[4 * tid + 3]);
         }
         if (tid == 0) {
             int2 &sa = p.stats[(size_t)inst * K + a_upd];
@@ -783,6 +795,7 @@ struct InitArgs {
     uint32_t *mask;
     int32_t *inst;
     int2 *stats;
+    float4 *theta;        // [B][K][d/4] or nullptr
     StateHeader *hdr;
     StateHeader h;
     int32_t B, K, KW, d, C, IW;
@@ -816,6 +829,9 @@ __global__ void agft_init_kernel(InitArgs p) {
         p.mask[idx] = rem >= 32 ? 0xffffffffu : ((1u << rem) - 1u);
     }
     for (size_t idx = gtid; idx < (size_t)p.B * p.K; idx += gsz) p.stats[idx] = make_int2(0, 0);
+    if (p.theta != nullptr)
+        for (size_t idx = gtid; idx < (size_t)p.B * p.K * (p.d / 4); idx += gsz)
+            p.theta[idx] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (size_t idx = gtid; idx < (size_t)p.B * p.IW; idx += gsz) {
         const int w = (int)(idx % p.IW);
         p.inst[idx] = w == kInstAprev || w == kInstMode ? -1
@@ -912,6 +928,7 @@ StateHeader make_header(const agft_config *c) {
     h.alpha_sched = c->alpha_sched;
     h.prune_rule = c->prune_rule;
     h.prune_period = c->prune_period;
+    h.exploit = c->exploit;
     return h;
 }
 
@@ -926,7 +943,7 @@ extern "C" {
 
 size_t agft_state_bytes(const agft_config *cfg) {
     if (!config_ok(cfg) || !dim_supported(cfg->d)) return 0;
-    return layout_for(cfg->B, cfg->K, cfg->d).total;
+    return layout_for(cfg->B, cfg->K, cfg->d, cfg->exploit).total;
 }
 
 int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stream, agft_handle **out) {
@@ -935,7 +952,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     if (!config_ok(cfg) || d_state == nullptr) return AGFT_E_INVAL;
     if (!dim_supported(cfg->d)) return AGFT_E_UNSUPPORTED;
     if (reinterpret_cast<uintptr_t>(d_state) % kAlign != 0) return AGFT_E_INVAL;
-    const Layout lay = layout_for(cfg->B, cfg->K, cfg->d);
+    const Layout lay = layout_for(cfg->B, cfg->K, cfg->d, cfg->exploit);
     if (nbytes < lay.total) return AGFT_E_INVAL;
     agft_handle *h = new (std::nothrow) agft_handle;
     if (h == nullptr) return AGFT_E_INVAL;
@@ -955,7 +972,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
             return AGFT_E_HIP;
         }
         if (got.magic != kMagic || got.version != want.version || got.B != want.B || got.K != want.K ||
-            got.d != want.d || got.chunks != want.chunks || got.t < 0 ||
+            got.d != want.d || got.chunks != want.chunks || got.exploit != want.exploit || got.t < 0 ||
             (got.pending != 0 && got.pending != 1)) {
             delete h;
             return AGFT_E_STATE;
@@ -970,6 +987,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     a.mask = at<uint32_t>(h->base, lay.mask);
     a.inst = at<int32_t>(h->base, lay.inst);
     a.stats = at<int2>(h->base, lay.stats);
+    a.theta = cfg->exploit ? at<float4>(h->base, lay.theta) : nullptr;
     a.hdr = at<StateHeader>(h->base, 0);
     a.h = want;
     a.B = cfg->B;
@@ -1002,6 +1020,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.mask = at<uint32_t>(h->base, h->lay.mask);
     p.inst = at<int32_t>(h->base, h->lay.inst);
     p.stats = at<int2>(h->base, h->lay.stats);
+    p.theta = c.exploit ? at<float>(h->base, h->lay.theta) : nullptr;
     p.h.mask = c.prune_rule & 14;
     p.h.ext_rounds = c.ext_rounds;
     p.h.ext_min_n = c.ext_min_n;
@@ -1063,6 +1082,7 @@ int agft_get_state(const agft_handle *h, agft_state_view *out) {
     out->inst = at<int32_t>(h->base, h->lay.inst);
     out->inst_words = inst_words(h->cfg.d);
     out->stats = at<int32_t>(h->base, h->lay.stats);
+    out->theta = h->cfg.exploit ? at<float>(h->base, h->lay.theta) : nullptr;
     return AGFT_OK;
 }
 

@@ -123,6 +123,7 @@ class Tuner:
             aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2], mode=inst[:, 3], ph=inst[:, 3:12],
             xprev=inst[:, 12:12 + d].view(torch.float32),
             stats=region(v.stats, B * K * 2, torch.int32, (B, K, 2)),
+            theta=region(v.theta, B * K * d, torch.float32, (B, K, d)) if v.theta else None,
         )
 
     @property

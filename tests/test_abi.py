@@ -65,8 +65,20 @@ def test_state_bytes(lib):
                 dict(prune_rule=2, ext_min_n=0), dict(prune_rule=2, ext_min_n=3, ext_thr=float("nan")),
                 dict(prune_rule=4, hist_min_n=0, hist_min_arms=3),
                 dict(prune_rule=4, hist_min_n=6, hist_min_arms=3, hist_kappa=-1.0),
-                dict(prune_rule=8, cascade_k=17)):
+                dict(prune_rule=8, cascade_k=17),
+                dict(exploit=2), dict(exploit=1, ph_lambda=-1.0), dict(exploit=1, ph_delta=float("nan")),
+                dict(exploit=1, ph_window=-1), dict(exploit=1, ph_min_rounds=-5)):
         assert L.agft_state_bytes(_cfg(**bad)) == 0, bad
+
+
+def test_state_bytes_with_exploitation(lib):
+    """The switch adds the contiguous theta copy, B*K*d floats."""
+    ph = dict(ph_delta=0.05, ph_lambda=5.0, ph_window=100, ph_min_rounds=100)
+    for B, K, d in ((4, 16, 8), (1000, 128, 16), (3, 1024, 32)):
+        off = L.agft_state_bytes(_cfg(B=B, K=K, d=d, **ph))
+        on = L.agft_state_bytes(_cfg(B=B, K=K, d=d, exploit=1, **ph))
+        copy = B * K * d * 4
+        assert copy <= on - off < copy + 256 and on % 256 == 0
 
 
 def test_create_rejects_before_launch(lib):
