@@ -69,7 +69,7 @@ def cpu_baseline(wl, budget_s):
     import numpy as np
     from agft_workloads import exogenous
     from oracle import Env, Oracle
-    n = min(wl.B, 4096)
+    n = min(wl.B, 16384)
     T = wl.T
     arr, noi = exogenous(wl, range(n), T)
     env = Env(wl, arr, noi, T)

@@ -134,12 +134,28 @@ Layout layout_for(int B, int K, int d, int exploit) {
     return L;
 }
 
-// Workgroup width for K arms of dimension d: enough groups of d/2 lanes for
-// all arms, at most 4 wavefronts (larger K loops over the arms).
-int waves_for(int K, int d) {
+// Dynamic LDS of the step kernel: UCB and LCB per arm, then the arm list.
+size_t step_lds_bytes(int K) { return ((size_t)K * (2 * 4 + 2) + 15) / 16 * 16; }
+
+// Workgroup width (wavefronts) for K arms of dimension d; one workgroup per
+// instance, looping over the arms in passes of 64*w/(d/2).  The step is a
+// chain of dependent phases per instance, so narrow workgroups (more
+// instances in flight per CU, cheaper barriers) win unless each instance
+// streams many whole records:
+//   1 when one wavefront covers the arms in at most 8 passes;
+//   2 at d = 32 (3 wavefronts per SIMD fit its registers, so 2-wave groups
+//     keep twice as many instances resident as 4-wave ones);
+//   1 when the switch to exploitation is on (exploiting instances read d
+//     floats per arm);
+//   4 otherwise.
+// Measured on MI355X (step kernel, us): K=64 d=8 B=4096: 21 / 25 / 30 for
+// w = 1 / 2 / 4; K=256 d=32 B=1024: 34 / 31 / 40; K=128 d=16 B=65536: 895 /
+// 892 / 882; the same with the switch on: 595 / 602 / 672.
+int waves_for(int K, int d, int exploit) {
     const int lanes = K * (d / 2);
-    int w = (lanes + kWave - 1) / kWave;
-    return w < 1 ? 1 : (w > 4 ? 4 : w);
+    if (lanes <= 8 * kWave) return 1;
+    if (d == 32) return 2;
+    return exploit ? 1 : 4;
 }
 
 // Per-lane slice of the Eq. 1 terms from the S chunks of one record slice:
@@ -276,9 +292,12 @@ void agft_step_kernel(StepArgs p) {
     __shared__ float s_ca[D];
     __shared__ float s_cb[D];
     __shared__ float s_scal[2];   // alpha_{d-1}, prediction error
-    __shared__ float s_ucb[kMaxK];
-    __shared__ float s_lcb[kMaxK];
-    __shared__ short s_list[kMaxK];
+    // per-arm scores and the list of arms to stream, sized by K at launch
+    // (step_lds_bytes) so that small arm counts leave room for more workgroups
+    extern __shared__ float s_arm[];
+    float *s_ucb = s_arm;
+    float *s_lcb = s_arm + K;
+    short *s_list = reinterpret_cast<short *>(s_arm + 2 * K);
     __shared__ uint32_t s_mask[kMaxWords];
     __shared__ int s_nlist;
     __shared__ float s_red_v[kMaxWaves];
@@ -1050,11 +1069,12 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
-    const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves_for(c.K, c.d)));
+    const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves_for(c.K, c.d, c.exploit)));
+    const size_t lds = step_lds_bytes(c.K);
     switch (c.d) {
-        case 8: hipLaunchKernelGGL(agft_step_kernel<8>, grid, block, 0, h->stream, p); break;
-        case 16: hipLaunchKernelGGL(agft_step_kernel<16>, grid, block, 0, h->stream, p); break;
-        case 32: hipLaunchKernelGGL(agft_step_kernel<32>, grid, block, 0, h->stream, p); break;
+        case 8: hipLaunchKernelGGL(agft_step_kernel<8>, grid, block, lds, h->stream, p); break;
+        case 16: hipLaunchKernelGGL(agft_step_kernel<16>, grid, block, lds, h->stream, p); break;
+        case 32: hipLaunchKernelGGL(agft_step_kernel<32>, grid, block, lds, h->stream, p); break;
         default: return AGFT_E_UNSUPPORTED;
     }
     const hipError_t e = hipGetLastError();
