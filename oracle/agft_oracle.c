@@ -20,7 +20,7 @@
  * alpha_t is alpha0 or alpha0 / sqrt(t + 1); ties go to the lowest arm index;
  * a negative rounding of the quadratic form is taken as 0 under the root.
  *
- * Pruning; every rule removes arms for good ("permanently removed", Sec. 4.3).
+ * Pruning; every rule removes arms for good (as Sec. 4.3 says of its own rules).
  * The rule set is a bit mask:
  *   1  confidence bounds: at a step t > 0 with t % period == 0, an active arm
  *      k stays active iff UCB_k >= max over the active arms j of LCB_j, all
