@@ -51,6 +51,17 @@ class Workload:
     ph_lambda: float = 5.0
     ph_window: int = 100
     ph_min_rounds: int = 100
+    # mixed-maturity refinement of the action space (Sec. 4.4): one arm step
+    # of the K-arm grid plays the paper's 15 MHz step, so its +-150 MHz window
+    # is +-10 arms (21 arms) and the coarse starting grid takes every 10th arm;
+    # maturity after 100 rounds and 4 samples for the statistical anchor are
+    # the paper's example values; the refinement period is unstated
+    refine: int = 0
+    refine_period: int = 50
+    refine_stride: int = 10
+    refine_half: int = 10
+    refine_mature: int = 100
+    refine_min_n: int = 4
 
     @property
     def arm_record_floats(self) -> int:
@@ -71,6 +82,11 @@ class Workload:
     def page_hinkley(self) -> dict:
         return dict(ph_delta=self.ph_delta, ph_lambda=self.ph_lambda, ph_window=self.ph_window,
                     ph_min_rounds=self.ph_min_rounds)
+
+    def refinement(self) -> dict:
+        return dict(refine_period=self.refine_period, refine_stride=self.refine_stride,
+                    refine_half=self.refine_half, refine_mature=self.refine_mature,
+                    refine_min_n=self.refine_min_n)
 
     def alpha_at(self, t: int) -> float:
         if self.alpha_sched == 0:
@@ -120,6 +136,15 @@ def with_exploitation(wl: Workload) -> Workload:
     return Workload(**d)
 
 
+def with_refinement(wl: Workload) -> Workload:
+    """The same workload with the mixed-maturity refinement of the action space."""
+    d = dict(wl.__dict__)
+    d["refine"] = 1
+    d["name"] = wl.name + "r"
+    d["description"] = wl.description + ", plus the mixed-maturity refinement"
+    return Workload(**d)
+
+
 def get_workload(cfg, **overrides) -> Workload:
     """Workload by id (1..5) or name ("cfg4"), optionally with fields replaced
     (smaller B or T for quick parity cases)."""
@@ -128,13 +153,16 @@ def get_workload(cfg, **overrides) -> Workload:
         body = cfg.replace("cfg", "")
         suffix = body.lstrip("0123456789")
         cfg = int(body[:len(body) - len(suffix)])
-        if set(suffix) - set("pe"):
-            raise ValueError(f"unknown workload suffix {suffix!r} (p: paper pruning, e: exploitation)")
+        if set(suffix) - set("per"):
+            raise ValueError(f"unknown workload suffix {suffix!r} (p: paper pruning, "
+                             f"e: exploitation, r: refinement)")
     wl = WORKLOADS[cfg]
     if "p" in suffix:
         wl = with_paper_pruning(wl)
     if "e" in suffix:
         wl = with_exploitation(wl)
+    if "r" in suffix:
+        wl = with_refinement(wl)
     if overrides:
         d = dict(wl.__dict__)
         d.update(overrides)

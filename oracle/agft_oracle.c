@@ -55,6 +55,21 @@
  * The test decides an integer (the switch round), so it runs in single
  * precision with the GPU kernel's operation order; the model stays double.
  *
+ * Mixed-maturity refinement (Sec. 4.4), when enabled: the action space is a
+ * set of arms on the K-arm grid (one arm step plays the paper's 15 MHz),
+ * lo <= k <= hi with (hi - k) % stride == 0, intersected with the arms no
+ * pruning rule has removed.  It starts as the coarse grid lo = 0, hi = K-1,
+ * stride = refine_stride.  At a step t > 0 with t % refine_period == 0 that
+ * made a decision, after the decision, an anchor is chosen among the arms of
+ * the action space that survived this step's pruning: before round
+ * refine_mature the one with the best mean reward (the lowest mean EDP)
+ * among those with at least refine_min_n rewards (lowest index on ties; no
+ * refinement if none qualifies), from then on the arm this step chose (the
+ * highest UCB, or theta^T x once exploiting).  The action space becomes the
+ * full-resolution window lo = max(0, anchor - refine_half), hi = min(K-1,
+ * anchor + refine_half), stride 1, from the next step on.  Every arm keeps
+ * its model across refinements; pruned arms stay pruned.
+ *
  * Step order: the reward r_{t-1} of the previous decision arrives with the
  * next context, so ora_decide first applies Eq. 3-5 to the arm chosen at
  * t-1 with (x_{t-1}, r_{t-1}), then scores x_t, prunes and picks a_t.
@@ -85,6 +100,9 @@ typedef struct {
     int exploit, ph_window, ph_min_rounds;
     float ph_delta, ph_lambda;
     float *ph;              /* [B][6]        n, mean, m+, min m+, m-, min m- */
+    /* mixed-maturity refinement */
+    int refine, refine_period, refine_stride, refine_half, refine_mature, refine_min_n;
+    int *win;               /* [B][3]        action space lo, hi, stride */
     float *ph_margin;       /* [B]           lambda - larger statistic at the last test */
     long *ph_last;          /* [B]           round of the last alarm (0 at start) */
     long *mode;             /* [B]           -1 exploring, else the round exploitation began */
@@ -92,7 +110,7 @@ typedef struct {
     double *b;              /* [B][K][d]     Eq. 4 */
     double *Ainv;           /* [B][K][d][d]  inverse of A */
     double *theta;          /* [B][K][d]     Eq. 5 */
-    unsigned char *active;  /* [B][K]        current action set */
+    unsigned char *active;  /* [B][K]        arms no pruning rule has removed */
     int *nsel;              /* [B][K]        rewards folded into each arm */
     double *rsum;           /* [B][K]        sum of those rewards */
     double *xprev;          /* [B][d]        context of the last decision */
@@ -141,6 +159,9 @@ void ora_get_rsum(const void *h, int i, double *rsum);
 void ora_set_exploit(void *h, int on, double delta, double lambda, int window, int min_rounds);
 void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, long *mode);
 void ora_set_ph(void *h, int i, const float *stats, float margin, long last, long mode);
+void ora_set_refine(void *h, int on, int period, int stride, int half, int mature, int min_n);
+void ora_get_window(const void *h, int i, int *lo, int *hi, int *stride);
+void ora_set_window(void *h, int i, int lo, int hi, int stride);
 
 static int all_finite(const double *v, int n)
 {
@@ -173,11 +194,12 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
     o->ph_margin = (float *)malloc((size_t)B * sizeof(float));
     o->ph_last = (long *)calloc((size_t)B, sizeof(long));
     o->mode = (long *)malloc((size_t)B * sizeof(long));
-    if (!o->A || !o->b || !o->Ainv || !o->theta || !o->active || !o->nsel || !o->rsum ||
+    o->win = (int *)malloc((size_t)B * 3 * sizeof(int));
+    if (!o->win || !o->A || !o->b || !o->Ainv || !o->theta || !o->active || !o->nsel || !o->rsum ||
         !o->xprev || !o->aprev || !o->bad || !o->ph || !o->ph_margin || !o->ph_last || !o->mode) {
         free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
         free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad);
-        free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o);
+        free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o->win); free(o);
         return NULL;
     }
     /* A_k(0) = lambda I, b_k(0) = 0, hence A_k^{-1}(0) = I / lambda, theta_k(0) = 0. */
@@ -191,6 +213,9 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
         o->aprev[i] = -1;
         o->mode[i] = -1;
         o->ph_margin[i] = INFINITY;
+        o->win[3 * i] = 0;
+        o->win[3 * i + 1] = K - 1;
+        o->win[3 * i + 2] = 1;
     }
     return o;
 }
@@ -201,7 +226,51 @@ void ora_destroy(void *h)
     if (!o) return;
     free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
     free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad);
-    free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o);
+    free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o->win); free(o);
+}
+
+/* Refinement: on/off and its parameters (see the header); call before the
+ * first decision.  Every instance starts on the coarse grid. */
+void ora_set_refine(void *h, int on, int period, int stride, int half, int mature, int min_n)
+{
+    ora_t *o = (ora_t *)h;
+    o->refine = on;
+    o->refine_period = period;
+    o->refine_stride = stride;
+    o->refine_half = half;
+    o->refine_mature = mature;
+    o->refine_min_n = min_n;
+    for (int i = 0; i < o->B; ++i) {
+        o->win[3 * i] = 0;
+        o->win[3 * i + 1] = o->K - 1;
+        o->win[3 * i + 2] = on ? stride : 1;
+    }
+}
+
+/* Action space of instance i (lo, hi, stride); outputs may be NULL. */
+void ora_get_window(const void *h, int i, int *lo, int *hi, int *stride)
+{
+    const ora_t *o = (const ora_t *)h;
+    if (lo) *lo = o->win[3 * i];
+    if (hi) *hi = o->win[3 * i + 1];
+    if (stride) *stride = o->win[3 * i + 2];
+}
+
+/* Overwrite instance i's action space (the parity harness adopts the GPU's
+ * where two anchor candidates were within rounding of each other). */
+void ora_set_window(void *h, int i, int lo, int hi, int stride)
+{
+    ora_t *o = (ora_t *)h;
+    o->win[3 * i] = lo;
+    o->win[3 * i + 1] = hi;
+    o->win[3 * i + 2] = stride;
+}
+
+/* Arm k is in instance i's action space (before pruning). */
+static int in_space(const ora_t *o, int i, int k)
+{
+    const int lo = o->win[3 * i], hi = o->win[3 * i + 1], st = o->win[3 * i + 2];
+    return k >= lo && k <= hi && (hi - k) % st == 0;
 }
 
 /* Exploitation switch: on/off and the Page-Hinkley parameters (see the header). */
@@ -370,9 +439,10 @@ double ora_alpha(const void *h, long t)
  * One decision for every instance.
  *   x      [B][d] context x_t
  *   r      [B]    reward of the previous decision (may be NULL when none is pending)
- *   ucb, lcb [B][K] out: scores of the arms active before this step's pruning,
- *                   -INFINITY for arms already inactive
- *   keep   [B][K] out: action set after this step's pruning
+ *   ucb, lcb [B][K] out: scores of the arms of the action space after rules
+ *                   2-8 (before rule 1), -INFINITY for the others
+ *   keep   [B][K] out: arms no pruning rule has removed, after this step's
+ *                   pruning (the refinement window is not applied to it)
  *   action [B]    out: a_t, or -1 when x_t is not finite
  * The state's action set and last decision are not changed here: see ora_commit.
  */
@@ -396,12 +466,16 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
     for (int i = 0; i < B; ++i) {
         if (pending) apply_pending(o, i, r);
         const double *xi = x + (size_t)i * d;
-        unsigned char act1[1024];
+        unsigned char act0[1024], act1[1024];
         double marg[1024];
-        const unsigned char *act = o->active + (size_t)i * K;
+        const unsigned char *glob = o->active + (size_t)i * K;
         double *U = ucb + (size_t)i * K, *L = lcb + (size_t)i * K;
         unsigned char *kp = keep + (size_t)i * K;
-        for (int k = 0; k < K; ++k) { U[k] = -INFINITY; L[k] = -INFINITY; kp[k] = act[k]; marg[k] = INFINITY; }
+        for (int k = 0; k < K; ++k) {
+            U[k] = -INFINITY; L[k] = -INFINITY; kp[k] = glob[k]; marg[k] = INFINITY;
+            act0[k] = glob[k] && in_space(o, i, k);
+        }
+        const unsigned char *act = act0;   /* the action space: not pruned, in the window */
         if (!all_finite(xi, d)) {
             o->bad[i] += 1;
             action[i] = -1;
@@ -410,8 +484,9 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
         }
         if (o->prune & 14) {
             heuristic_prune(o, i, t, act, act1, marg);
+            for (int k = 0; k < K; ++k)
+                if (act0[k] && !act1[k]) kp[k] = 0;
             act = act1;
-            for (int k = 0; k < K; ++k) kp[k] = act[k];
         }
         if (margins) memcpy(margins + (size_t)i * K, marg, sizeof(double) * K);
         if (o->exploit && o->mode[i] < 0 && t >= o->ph_min_rounds && t - o->ph_last[i] >= o->ph_window)
@@ -441,21 +516,48 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
         }
         int best = -1;
         for (int k = 0; k < K; ++k)
-            if (kp[k] && (best < 0 || U[k] > U[best])) best = k;
+            if (act[k] && kp[k] && (best < 0 || U[k] > U[best])) best = k;
         action[i] = best;
     }
     o->pending = 0;
 }
 
-/* Record the decision taken at this step: x_t, a_t and the action set. */
+/* Refinement of instance i's action space after the decision a of step t. */
+static void refine_space(ora_t *o, int i, long t, int a)
+{
+    const int K = o->K;
+    const unsigned char *glob = o->active + (size_t)i * K;
+    const int *n = o->nsel + (size_t)i * K;
+    const double *rs = o->rsum + (size_t)i * K;
+    int anchor = -1;
+    if (t < o->refine_mature) {
+        /* statistical: best mean reward (lowest mean EDP), enough samples */
+        for (int k = 0; k < K; ++k)
+            if (glob[k] && in_space(o, i, k) && n[k] >= o->refine_min_n &&
+                (anchor < 0 || rs[k] / n[k] > rs[anchor] / n[anchor]))
+                anchor = k;
+    } else {
+        anchor = a;   /* predictive: this step's UCB (or Eq. 2) argmax */
+    }
+    if (anchor < 0) return;
+    o->win[3 * i] = anchor - o->refine_half > 0 ? anchor - o->refine_half : 0;
+    o->win[3 * i + 1] = anchor + o->refine_half < K - 1 ? anchor + o->refine_half : K - 1;
+    o->win[3 * i + 2] = 1;
+}
+
+/* Record the decision taken at this step: x_t, a_t and the arms no pruning
+ * rule has removed; then refine the action space when due. */
 void ora_commit(void *h, const double *x, const int *action, const unsigned char *keep)
 {
     ora_t *o = (ora_t *)h;
     const int B = o->B, K = o->K, d = o->d;
+    const long t = o->t;
+    const int refine_now = o->refine && t > 0 && (t % o->refine_period) == 0;
     for (int i = 0; i < B; ++i) {
         memcpy(o->xprev + (size_t)i * d, x + (size_t)i * d, sizeof(double) * d);
         o->aprev[i] = action[i];
         if (keep) memcpy(o->active + (size_t)i * K, keep + (size_t)i * K, K);
+        if (refine_now && action[i] >= 0) refine_space(o, i, t, action[i]);
     }
     o->t += 1;
     o->pending = 1;

@@ -36,6 +36,9 @@ def _declare(lib):
     lib.ora_set_exploit.argtypes = [P, I, D, D, I, I]
     lib.ora_get_ph.argtypes = [P, I, P, P, P, P]
     lib.ora_set_ph.argtypes = [P, I, P, ctypes.c_float, L, L]
+    lib.ora_set_refine.argtypes = [P, I, I, I, I, I, I]
+    lib.ora_get_window.argtypes = [P, I, P, P, P]
+    lib.ora_set_window.argtypes = [P, I, I, I, I]
     lib.ora_commit.argtypes = [P, P, P, P]
     lib.ora_flush.argtypes = [P, P]
     lib.ora_get.argtypes = [P, I, P, P, P, P, P, P, P]
@@ -84,6 +87,8 @@ class Oracle:
             o.set_heuristics(**wl.heuristics())
         if wl.exploit:
             o.set_exploit(True, **wl.page_hinkley())
+        if wl.refine:
+            o.set_refine(True, **wl.refinement())
         return o
 
     def set_exploit(self, on, ph_delta, ph_lambda, ph_window, ph_min_rounds):
@@ -100,6 +105,21 @@ class Oracle:
         self.lib.ora_get_ph(self.h, int(i), _ptr(stats), ctypes.byref(margin), ctypes.byref(last),
                             ctypes.byref(mode))
         return stats, margin.value, last.value, mode.value
+
+    def set_refine(self, on, refine_period, refine_stride, refine_half, refine_mature,
+                   refine_min_n):
+        """Mixed-maturity refinement of the action space (Sec. 4.4)."""
+        self.lib.ora_set_refine(self.h, int(bool(on)), int(refine_period), int(refine_stride),
+                                int(refine_half), int(refine_mature), int(refine_min_n))
+
+    def window(self, i):
+        """(lo, hi, stride) of instance i's action space."""
+        v = [ctypes.c_int(0) for _ in range(3)]
+        self.lib.ora_get_window(self.h, int(i), *(ctypes.byref(q) for q in v))
+        return tuple(q.value for q in v)
+
+    def set_window(self, i, lo, hi, stride):
+        self.lib.ora_set_window(self.h, int(i), int(lo), int(hi), int(stride))
 
     def set_page_hinkley(self, i, stats, margin, last, mode):
         """Overwrite instance i's Page-Hinkley state and mode."""

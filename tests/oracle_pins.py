@@ -536,3 +536,156 @@ def pin_greedy_after_switch(lib):
 
 
 ALL_PINS += [pin_page_hinkley_switch_round, pin_greedy_after_switch]
+
+
+# ---- mixed-maturity refinement of the action space (Sec. 4.4) ----
+
+def _in_space(k, lo, hi, stride):
+    return lo <= k <= hi and (hi - k) % stride == 0
+
+
+def _brute_refine_trajectory(lib, B, K, d, T, stride, half, period, mature, min_n, prune, pperiod,
+                             seed, alpha0=0.6):
+    """Drive the oracle with refinement on and check every step against an
+    independent restatement: the action space as an explicit set, scores by
+    direct solve from each arm's full history (models persist while an arm is
+    outside the space), rule 1, the argmax, and the anchor chosen after the
+    decision (best mean reward with enough samples before maturity, the
+    decision itself after).  Returns the number of arms that re-entered the
+    space with a history of their own."""
+    rng = np.random.default_rng(seed)
+    xs = _rand_contexts(rng, T, B, d)
+    rs = rng.uniform(-2.0, 0.0, size=(T, B))
+    ora = Oracle(B, K, d, 1.0, alpha0, 0, prune, pperiod, lib=lib)
+    ora.set_refine(True, period, stride, half, mature, min_n)
+    hist = [[[] for _ in range(K)] for _ in range(B)]
+    pruned = np.zeros((B, K), dtype=bool)
+    win = [(0, K - 1, stride) for _ in range(B)]
+    seen_out = np.zeros((B, K), dtype=bool)
+    reentries = 0
+    r_prev = None
+    for t in range(T):
+        ucb, lcb, keep, action = ora.decide(xs[t], r_prev)
+        for i in range(B):
+            lo, hi, st = win[i]
+            space = [k for k in range(K) if _in_space(k, lo, hi, st) and not pruned[i, k]]
+            for k in range(K):
+                if k in space:
+                    if seen_out[i, k] and hist[i][k]:
+                        reentries += 1
+                        seen_out[i, k] = False
+                    _, _, _, U, L = _brute_scores(hist[i][k], 1.0, d, xs[t, i], alpha0)
+                    assert abs(ucb[i, k] - U) <= 1e-9 * max(1.0, abs(U)), (t, i, k)
+                    assert abs(lcb[i, k] - L) <= 1e-9 * max(1.0, abs(L)), (t, i, k)
+                else:
+                    assert ucb[i, k] == -np.inf, (t, i, k)
+                    seen_out[i, k] = True
+            survivors = list(space)
+            if prune and t > 0 and t % pperiod == 0:
+                lstar = max(lcb[i, k] for k in space)
+                survivors = [k for k in space if not ucb[i, k] < lstar]
+                for k in space:
+                    if k not in survivors:
+                        pruned[i, k] = True
+            assert (keep[i] == ~pruned[i]).all(), (t, i)
+            best = max(survivors, key=lambda k: (ucb[i, k], -k))
+            assert action[i] == best, (t, i, action[i], best)
+            hist[i][best].append((xs[t, i], rs[t, i]))
+            if t > 0 and t % period == 0:
+                if t < mature:
+                    # the means count the rewards folded in so far, not this step's
+                    means = {k: sum(q for _, q in hist[i][k][:len(hist[i][k]) - (k == best)])
+                             / (len(hist[i][k]) - (k == best)) for k in survivors
+                             if len(hist[i][k]) - (k == best) >= min_n}
+                    anchor = max(means, key=lambda k: (means[k], -k)) if means else None
+                else:
+                    anchor = best
+                if anchor is not None:
+                    win[i] = (max(0, anchor - half), min(K - 1, anchor + half), 1)
+        ora.commit(xs[t], action, keep)
+        for i in range(B):
+            assert ora.window(i) == win[i], (t, i, ora.window(i), win[i])
+        r_prev = rs[t]
+    return reentries
+
+
+def pin_refinement_brute_force(lib):
+    """Refinement with coarse grids, moving windows, rule 1 and re-entering
+    arms, against the explicit restatement above."""
+    n = _brute_refine_trajectory(lib, B=2, K=12, d=2, T=60, stride=3, half=2, period=4, mature=20,
+                                 min_n=2, prune=1, pperiod=7, seed=11)
+    n += _brute_refine_trajectory(lib, B=2, K=20, d=3, T=70, stride=4, half=1, period=3, mature=30,
+                                  min_n=1, prune=0, pperiod=5, seed=12)
+    n += _brute_refine_trajectory(lib, B=1, K=9, d=4, T=50, stride=2, half=3, period=5, mature=10,
+                                  min_n=3, prune=1, pperiod=4, seed=13)
+    assert n > 0, "no arm re-entered the action space with a history"
+
+
+def pin_refinement_coarse_sweep(lib):
+    """Untouched arms tie exactly, so the first decisions sweep the coarse grid
+    in index order; the grid is counted down from the top arm."""
+    K, d = 40, 2
+    ora = Oracle(1, K, d, 1.0, 1.0, 0, 0, 50, lib=lib)
+    ora.set_refine(True, 100, 10, 10, 100, 4)
+    x = np.array([[1.0, 0.5]])
+    acts = []
+    r_prev = None
+    for t in range(4):
+        ucb, lcb, keep, action = ora.decide(x, r_prev)
+        if t == 0:
+            assert np.isfinite(ucb[0]).sum() == 4
+        acts.append(int(action[0]))
+        ora.commit(x, action, keep)
+        r_prev = np.array([-1.0])
+    assert acts == [9, 19, 29, 39], acts
+
+
+def pin_refinement_statistical_then_predictive(lib):
+    """A scripted reward that depends only on the arm: before maturity the
+    window centres on the coarse arm with the best mean reward once it has
+    enough samples; at maturity it centres on that step's choice."""
+    K, d = 60, 2
+    ora = Oracle(1, K, d, 1.0, 0.0, 0, 0, 50, lib=lib)      # alpha = 0: greedy on theta
+    ora.set_refine(True, 10, 10, 4, 30, 2)
+    reward = lambda k: -1.0 - abs(k - 33) / 20.0      # best coarse arm: 29 (grid 9, 19, ..., 59)
+    x = np.array([[1.0, 0.0]])
+    r_prev = None
+    for t in range(31):
+        ucb, lcb, keep, action = ora.decide(x, r_prev)
+        a = int(action[0])
+        ora.commit(x, action, keep)
+        r_prev = np.array([reward(a)])
+        if t == 10:
+            st = ora.get(0)
+            n, rsum = st["nsel"], st["rsum"]
+            cand = [k for k in range(9, K, 10) if n[k] >= 2]
+            assert 29 in cand
+            assert ora.window(0) == (25, 33, 1)
+        if t == 30:
+            assert ora.window(0) == (max(0, a - 4), min(K - 1, a + 4), 1)
+
+
+def pin_refinement_skips_pruned_arms(lib):
+    """The statistical anchor is taken among arms still in play: an arm that a
+    cascade removed does not anchor the window, however good its mean."""
+    K, d = 6, 2
+    ora = Oracle(1, K, d, 1.0, 1.0, 0, 2 | 8, 50, lib=lib)
+    ora.set_heuristics(ext_rounds=60, ext_min_n=1, ext_thr=-1.2, hist_after=1000, hist_min_n=100,
+                       hist_kappa=1.0, hist_min_arms=3, cascade_k=4)
+    ora.set_refine(True, 6, 1, 1, 100, 1)
+    reward = {0: -1.0, 1: -0.5, 2: -1.0, 3: -3.0, 4: -1.0, 5: -1.0}
+    x = np.array([[1.0, 0.0]])
+    r_prev = None
+    acts = []
+    for t in range(7):
+        ucb, lcb, keep, action = ora.decide(x, r_prev)
+        acts.append(int(action[0]))
+        ora.commit(x, action, keep)
+        r_prev = np.array([reward[acts[-1]]])
+    assert acts[:6] == [0, 1, 2, 3, 4, 5], acts
+    assert list(keep[0]) == [0, 0, 0, 0, 1, 1]
+    assert ora.window(0) == (3, 5, 1), ora.window(0)
+
+
+ALL_PINS += [pin_refinement_brute_force, pin_refinement_coarse_sweep,
+             pin_refinement_statistical_then_predictive, pin_refinement_skips_pruned_arms]

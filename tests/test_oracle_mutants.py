@@ -11,7 +11,8 @@ from oracle.oracle import _SRC
 
 # Pruning at t = 0 as well is not listed: every arm is still in its initial
 # state then, all scores tie, and the prune cannot remove anything, so that
-# change is equivalent rather than a mistake.
+# change is equivalent rather than a mistake.  Nor is dropping the action-space
+# test from the argmax: arms outside the space score -inf, below any arm inside.
 MUTANTS = {
     "eq3_dropped_outer_product": ("A[p * d + q] += x[p] * x[q];", "A[p * d + q] += x[p] * x[p];"),
     "eq4_wrong_sign": ("b[p] += r * x[p];", "b[p] -= r * x[p];"),
@@ -50,6 +51,18 @@ MUTANTS = {
     "ph_window_off_by_one": ("t - o->ph_last[i] >= o->ph_window", "t - o->ph_last[i] > o->ph_window"),
     "ph_min_rounds_ignored": ("t >= o->ph_min_rounds && ", ""),
     "greedy_scores_with_bonus": ("U[k] = greedy ? m : m + alpha * w;", "U[k] = m + alpha * w;"),
+    "coarse_grid_from_bottom": ("return k >= lo && k <= hi && (hi - k) % st == 0;",
+                                "return k >= lo && k <= hi && (k - lo) % st == 0;"),
+    "refine_min_samples_off_by_one": ("n[k] >= o->refine_min_n", "n[k] > o->refine_min_n"),
+    "refine_anchor_worst_mean": ("rs[k] / n[k] > rs[anchor] / n[anchor]",
+                                 "rs[k] / n[k] < rs[anchor] / n[anchor]"),
+    "refine_predictive_from_maturity_plus_one": ("if (t < o->refine_mature) {", "if (t <= o->refine_mature) {"),
+    "refine_window_one_sided": ("o->win[3 * i] = anchor - o->refine_half > 0 ? anchor - o->refine_half : 0;",
+                                "o->win[3 * i] = anchor;"),
+    "refine_keeps_coarse_stride": ("    o->win[3 * i + 2] = 1;\n}", "    o->win[3 * i + 2] = o->refine_stride;\n}"),
+    "refine_period_off_by_one": ("(t % o->refine_period) == 0", "((t + 1) % o->refine_period) == 0"),
+    "refine_candidates_include_pruned": ("if (glob[k] && in_space(o, i, k) && n[k] >= o->refine_min_n &&",
+                                         "if (in_space(o, i, k) && n[k] >= o->refine_min_n &&"),
 }
 
 
