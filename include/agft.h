@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define AGFT_ABI_VERSION 2
+#define AGFT_ABI_VERSION 3
 
 enum agft_status {
     AGFT_OK = 0,
@@ -108,6 +108,24 @@ typedef struct agft_config {
     float ph_lambda;       /* finite, >= 0 */
     int32_t ph_window;     /* >= 0 */
     int32_t ph_min_rounds; /* >= 0 */
+    /* mixed-maturity refinement of the action space (Sec. 4.4): 0 off, 1 on.
+       The action space is lo <= k <= hi with (hi - k) % stride == 0, minus the
+       arms a pruning rule removed; it starts as the coarse grid lo = 0,
+       hi = K-1, stride = refine_stride (stride 1 when off).  At a step t > 0
+       with t % refine_period == 0 that decides, after the decision, an anchor
+       is taken among the arms of the space that survived the step's pruning:
+       before round refine_mature the best mean reward among the arms with at
+       least refine_min_n rewards (lowest index on ties; none qualifying: no
+       change), from then on the arm just chosen.  From the next step the
+       space is the full-resolution window [anchor - refine_half,
+       anchor + refine_half] clipped to [0, K-1].  Models persist for every
+       arm whether in the space or not. */
+    int32_t refine;
+    int32_t refine_period; /* >= 1 */
+    int32_t refine_stride; /* >= 1 */
+    int32_t refine_half;   /* >= 0 */
+    int32_t refine_mature; /* >= 0 */
+    int32_t refine_min_n;  /* >= 1 */
 } agft_config;
 
 typedef struct agft_handle agft_handle;
@@ -128,15 +146,18 @@ typedef struct agft_state_view {
                              e = d+1, d+2:  theta_{2j}, theta_{2j+1}
                              e > d+2:       0
                            with S upper triangular, S S^T = A^{-1}. */
-    uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k active */
+    uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k not
+                           removed by a pruning rule (the action space is apart) */
     int32_t *inst;      /* [B][inst_words] per-instance block of 32-bit words:
-                           [0] last decision (-1: none), [1] number of active arms,
+                           [0] last decision (-1: none), [1] arms in play (in the
+                           action space and not removed by a rule),
                            [2] non-finite contexts or rewards met,
                            [3] -1 while exploring, else the round exploitation began,
                            [4..9] Page-Hinkley n, mean, m+, min m+, m-, min m- (fp32),
                            [10] round of its last alarm, [11] its last margin (fp32),
-                           [12 .. 12+d) context of the last decision (fp32) */
-    int32_t inst_words; /* words per instance block: 12 + d rounded up to 16 */
+                           [12] [13] [14] action space lo, hi, stride, [15] reserved,
+                           [16 .. 16+d) context of the last decision (fp32) */
+    int32_t inst_words; /* words per instance block: 16 + d rounded up to 16 */
     int32_t *stats;     /* [B][K][2] per arm: [0] rewards folded in (int32),
                            [1] their sum (fp32 bits) */
     float *theta;       /* [B][K][d] copy of theta_k (Eq. 5), kept in step with the

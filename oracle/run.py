@@ -9,7 +9,7 @@ from .oracle import Oracle
 
 
 def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, lib=None,
-                    margins=False, on_create=None):
+                    margins=False, on_create=None, on_commit=None):
     """Run T decisions of len(instances) tuners against the fp64 environment.
 
     arrivals, noise: [T+1][n] exogenous draws (agft_workloads.exogenous).
@@ -19,7 +19,8 @@ def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, l
     of the pruning-rule comparisons from their thresholds.
     Returns a dict with the oracle object, actions [T][n] and, if record is
     set, contexts [T][n][d], rewards [T][n] (reward of decision t) and
-    ucb/lcb [T][n][K].  on_create(oracle) is called once the oracle exists.
+    ucb/lcb [T][n][K].  on_create(oracle) is called once the oracle exists,
+    on_commit(t) after each decision is committed.
     """
     T = wl.T if T is None else int(T)
     env = Env(wl, arrivals, noise, T)
@@ -42,6 +43,8 @@ def run_closed_loop(wl, arrivals, noise, T=None, on_decide=None, record=False, l
             if over is not None:
                 action, keep = over
         ora.commit(x, action, keep)
+        if on_commit is not None:
+            on_commit(t)
         actions[t] = action
         if record:
             rec["x"].append(x.copy()); rec["ucb"].append(ucb); rec["lcb"].append(lcb)

@@ -29,7 +29,9 @@ class agft_config(ctypes.Structure):
                 ("hist_after", _i32), ("hist_min_n", _i32), ("hist_kappa", _f32),
                 ("hist_min_arms", _i32), ("cascade_k", _i32),
                 ("exploit", _i32), ("ph_delta", _f32), ("ph_lambda", _f32),
-                ("ph_window", _i32), ("ph_min_rounds", _i32)]
+                ("ph_window", _i32), ("ph_min_rounds", _i32),
+                ("refine", _i32), ("refine_period", _i32), ("refine_stride", _i32),
+                ("refine_half", _i32), ("refine_mature", _i32), ("refine_min_n", _i32)]
 
 
 class agft_state_view(ctypes.Structure):
@@ -48,7 +50,7 @@ class agft_env_config(ctypes.Structure):
                 ("mu", _f32 * 7), ("sd", _f32 * 7)]
 
 
-ABI_VERSION = 2   # AGFT_ABI_VERSION of the agft_config layout declared here
+ABI_VERSION = 3   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
             "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version",

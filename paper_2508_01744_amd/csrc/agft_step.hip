@@ -11,17 +11,22 @@
 // contiguous matters for the update: rewriting one arm touches a handful of
 // cache lines instead of one line per 16-byte piece.
 //
-// Per step and instance (Sec. 4.2):
-//   1. fetch the record of the previous decision's arm (its update waits)
-//      and list the other active arms (the list skips pruned arms);
+// Per step and instance (Sec. 4.2-4.4):
+//   0. with the switch to exploitation on, feed the previous reward to the
+//      instance's Page-Hinkley test and switch when the rewards are stable;
+//   1. fetch the record of the previous decision's arm (its update waits);
+//      with the paper's pruning rules on, drop arms by their reward counts
+//      and means; list the other arms in play (in the action space, not
+//      pruned);
 //   2. every listed arm: m = theta^T x_t, w^2 = |S^T x_t|^2,
-//      UCB = m + alpha_t w, LCB = m - alpha_t w  (Eq. 1);
+//      UCB = m + alpha_t w, LCB = m - alpha_t w  (Eq. 1); an exploiting
+//      instance reads only a contiguous copy of theta and scores m (Eq. 2);
 //   3. fold the previous decision's reward into its arm: Eq. 3-5 as a
 //      square-root rank-1 update of S (below) plus the matching theta
 //      update, staged in LDS and written back; the updated arm is scored on
 //      x_t from LDS in the same operation order as the stream;
 //   4. pruning when due (drop UCB_k < max_j LCB_j), argmax with ties to the
-//      lowest arm index, epilogue.
+//      lowest arm index; refinement of the action space when due; epilogue.
 //
 // Square-root update.  Eq. 3 adds x x^T to A, so P = A^{-1} changes by the
 // Sherman-Morrison identity P' = P - P x x^T P / (1 + x^T P x).  With P = S S^T
@@ -108,10 +113,12 @@ __device__ inline void unpack(int e, int &i, int &j) {
 // Per-instance block of 32-bit words: previous action, active-arm count,
 // non-finite-input count, mode (-1 exploring, else the round exploitation
 // began), the Page-Hinkley state (n, mean, m+, min m+, m-, min m-), the round
-// of its last alarm, its last margin, then the stashed context.  Kept
-// together so the epilogue writes one or two lines per instance.
+// of its last alarm, its last margin, the action space (lo, hi, stride), a
+// spare word, then the stashed context.  Kept together so the epilogue
+// writes one or two lines per instance.
 constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstMode = 3, kInstPh = 4,
-              kInstPhLast = 10, kInstPhMargin = 11, kInstX = 12;
+              kInstPhLast = 10, kInstPhMargin = 11, kInstLo = 12, kInstHi = 13, kInstStride = 14,
+              kInstX = 16;
 
 int inst_words(int d) { return (kInstX + d + 15) / 16 * 16; }
 
@@ -192,6 +199,26 @@ struct Heuristics {
     int32_t hist_min_arms, cascade_k;
 };
 
+// Bits of word w of the action space lo <= k <= hi, (hi - k) % stride == 0.
+__device__ inline uint32_t space_bits(int w, int lo, int hi, int stride) {
+    const int k0 = 32 * w;
+    const int first = lo > k0 ? lo - k0 : 0;
+    const int last = hi < k0 + 31 ? hi - k0 : 31;
+    if (last < first) return 0u;
+    const uint32_t range = last - first == 31 ? 0xffffffffu : ((1u << (last - first + 1)) - 1u) << first;
+    if (stride == 1) return range;
+    uint32_t grid = 0u;   // positions congruent to hi modulo the stride
+    for (int b = (hi - k0) % stride; b < 32; b += stride) grid |= 1u << b;
+    return range & grid;
+}
+
+// Refinement of the action space after this step's decision (Sec. 4.4).
+struct Refine {
+    int32_t now;          // refinement due at this step
+    int32_t stat;         // statistical anchor (before maturity), else predictive
+    int32_t half, min_n;  // window half-width in arms; samples for the statistical anchor
+};
+
 // Switch to greedy exploitation after a Page-Hinkley test finds the
 // reward sequence stable (Sec. 4.2, Eq. 2).
 struct Exploit {
@@ -208,6 +235,7 @@ struct StepArgs {
     float *theta;         // [B][K][D] copy of theta (exploitation on), else nullptr
     Heuristics h;
     Exploit e;
+    Refine rf;
     int64_t t;            // decisions made before this step
     StateHeader *hdr;
     const float *ctx;     // [B][D] or nullptr (flush)
@@ -304,6 +332,9 @@ void agft_step_kernel(StepArgs p) {
     __shared__ int s_red_k[kMaxWaves];
     __shared__ int s_red_n[kMaxWaves];
     __shared__ uint32_t s_mask2[kMaxWords];
+    __shared__ uint32_t s_raw[kMaxWords];   // arms no rule has removed (the global mask words)
+    __shared__ float s_red_v2[kMaxWaves];
+    __shared__ int s_red_k2[kMaxWaves];
 
     const bool decide = p.ctx != nullptr;
 
@@ -367,8 +398,8 @@ void agft_step_kernel(StepArgs p) {
     // The block's words 3..11 after this step, parked in LDS by the lanes that
     // store them at the end (so they hold no registers through the stream; every
     // wave has read the old words before any lane writes the new ones).
-    __shared__ int s_phw[kInstX - kInstMode];
-    const bool ph_lane = p.e.on && tid >= kInstMode && tid < kInstX;
+    __shared__ int s_phw[kInstPhMargin + 1 - kInstMode];
+    const bool ph_lane = p.e.on && tid >= kInstMode && tid <= kInstPhMargin;
     if (ph_lane)
         s_phw[tid - kInstMode] = tid == kInstMode ? mode
                                : tid == kInstPhLast ? ph_last
@@ -386,7 +417,14 @@ void agft_step_kernel(StepArgs p) {
         }
     }
 
-    if (wave == 0 && lane < KW) s_mask[lane] = p.mask[(size_t)inst * KW + lane];
+    // the arms in play: not removed by a pruning rule, inside the action space
+    const int sp_lo = blk[kInstLo], sp_hi = blk[kInstHi];
+    const int sp_st = blk[kInstStride] > 1 ? blk[kInstStride] : 1;
+    if (wave == 0 && lane < KW) {
+        const uint32_t raw = p.mask[(size_t)inst * KW + lane];
+        s_raw[lane] = raw;
+        s_mask[lane] = raw & space_bits(lane, sp_lo, sp_hi, sp_st);
+    }
 
     // The paper's pruning rules (Sec. 4.3) on the arms active at step start,
     // with the previous decision's reward already counted.
@@ -494,7 +532,11 @@ void agft_step_kernel(StepArgs p) {
         __syncthreads();
         if (wave == 0 && lane < KW) {
             const uint32_t w = s_mask2[lane];
-            if (w != s_mask[lane]) p.mask[(size_t)inst * KW + lane] = w;
+            const uint32_t removed = s_mask[lane] & ~w;
+            if (removed != 0u) {
+                s_raw[lane] &= ~removed;
+                p.mask[(size_t)inst * KW + lane] = s_raw[lane];
+            }
             s_mask[lane] = w;
         }
         __syncthreads();
@@ -748,6 +790,8 @@ void agft_step_kernel(StepArgs p) {
         __syncthreads();
     }
     BestPair b{-INFINITY, 0x7fffffff};
+    BestPair sb{-INFINITY, 0x7fffffff};   // statistical refinement anchor
+    const bool stat_anchor = p.rf.now && p.rf.stat;
     int n = 0;
     float *sc = p.scores != nullptr ? p.scores + (size_t)inst * 2 * K : nullptr;
     for (int base = 0; base < K; base += nthr) {
@@ -758,28 +802,44 @@ void agft_step_kernel(StepArgs p) {
         if (keep) {
             b = better(b, BestPair{u, k});
             ++n;
+            if (stat_anchor) {
+                // best mean reward among the arms with enough rewards (this
+                // step's update already counted)
+                const int2 v = p.stats[(size_t)inst * K + k];
+                if (v.x >= p.rf.min_n) sb = better(sb, BestPair{__int_as_float(v.y) / (float)v.x, k});
+            }
         }
         if (sc != nullptr && k < K) {
             sc[k] = u;
             sc[K + k] = act ? s_lcb[k] : -INFINITY;
         }
         if (prune_now) {
+            // clear the arms rule 1 removed from the global words
             const unsigned long long bal = __ballot(keep);
             const int w0 = (base + wave * kWave) >> 5;
             uint32_t *mwo = p.mask + (size_t)inst * KW;
-            if (lane == 0 && w0 < KW) mwo[w0] = (uint32_t)(bal & 0xffffffffull);
-            if (lane == 0 && w0 + 1 < KW) mwo[w0 + 1] = (uint32_t)(bal >> 32);
+            if (lane == 0 && w0 < KW) {
+                s_raw[w0] &= ~(s_mask[w0] & ~(uint32_t)(bal & 0xffffffffull));
+                mwo[w0] = s_raw[w0];
+            }
+            if (lane == 0 && w0 + 1 < KW) {
+                s_raw[w0 + 1] &= ~(s_mask[w0 + 1] & ~(uint32_t)(bal >> 32));
+                mwo[w0 + 1] = s_raw[w0 + 1];
+            }
         }
     }
     for (int off = kWave / 2; off > 0; off >>= 1) {
         BestPair o{__shfl_xor(b.v, off), __shfl_xor(b.k, off)};
         b = better(b, o);
         n += __shfl_xor(n, off);
+        if (stat_anchor) sb = better(sb, BestPair{__shfl_xor(sb.v, off), __shfl_xor(sb.k, off)});
     }
     if (lane == 0) {
         s_red_v[wave] = b.v;
         s_red_k[wave] = b.k;
         s_red_n[wave] = n;
+        s_red_v2[wave] = sb.v;
+        s_red_k2[wave] = sb.k;
     }
     __syncthreads();
     if (wave == 0) {
@@ -792,6 +852,26 @@ void agft_step_kernel(StepArgs p) {
             cnt += s_red_n[w];
         }
         const int a = best.k == 0x7fffffff ? -1 : best.k;
+        // refinement after the decision: a window of 2*half+1 arms around the
+        // anchor, every arm at full resolution, from the next step on
+        int anchor = -1;
+        if (p.rf.now && a >= 0) {
+            if (p.rf.stat) {
+                BestPair sbest{s_red_v2[0], s_red_k2[0]};
+                for (int w = 1; w < nwave; ++w) sbest = better(sbest, BestPair{s_red_v2[w], s_red_k2[w]});
+                anchor = sbest.k == 0x7fffffff ? -1 : sbest.k;
+            } else {
+                anchor = a;
+            }
+        }
+        const int nlo = anchor - p.rf.half > 0 ? anchor - p.rf.half : 0;
+        const int nhi = anchor + p.rf.half < K - 1 ? anchor + p.rf.half : K - 1;
+        if (anchor >= 0) {
+            // arms in play in the new space
+            int c2 = lane < KW ? __popc(s_raw[lane] & space_bits(lane, nlo, nhi, 1)) : 0;
+            for (int off = kWave / 2; off > 0; off >>= 1) c2 += __shfl_xor(c2, off);
+            cnt = c2;
+        }
         if (lane == 0) {
             if (p.action != nullptr) p.action[inst] = a;
             if (inst == 0) {
@@ -801,6 +881,8 @@ void agft_step_kernel(StepArgs p) {
         }
         if (lane == kInstAprev) blk[kInstAprev] = a;
         if (lane == kInstKact) blk[kInstKact] = cnt;
+        if (anchor >= 0 && lane >= kInstLo && lane <= kInstStride)
+            blk[lane] = lane == kInstLo ? nlo : (lane == kInstHi ? nhi : 1);
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
         if (lane >= kInstX && lane < kInstX + D)
             reinterpret_cast<float *>(blk)[lane] = pick<D>(x, lane - kInstX);
@@ -818,6 +900,7 @@ struct InitArgs {
     StateHeader *hdr;
     StateHeader h;
     int32_t B, K, KW, d, C, IW;
+    int32_t stride0;      // stride of the starting action space
     float inv_sqrt_lambda;
 };
 
@@ -853,9 +936,13 @@ __global__ void agft_init_kernel(InitArgs p) {
             p.theta[idx] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (size_t idx = gtid; idx < (size_t)p.B * p.IW; idx += gsz) {
         const int w = (int)(idx % p.IW);
+        const int hi = p.K - 1;
+        const int kact0 = (hi - 0) / p.stride0 + 1;   // arms on the starting grid
         p.inst[idx] = w == kInstAprev || w == kInstMode ? -1
-                    : w == kInstKact ? p.K
+                    : w == kInstKact ? kact0
                     : w == kInstPhMargin ? 0x7f800000   // +inf: no test yet
+                    : w == kInstHi ? hi
+                    : w == kInstStride ? p.stride0
                     : 0;
     }
     if (gtid == 0) *p.hdr = p.h;
@@ -919,6 +1006,10 @@ bool config_ok(const agft_config *c) {
         return false;
     if ((c->prune_rule & 8) && (c->cascade_k < 0 || c->cascade_k > c->K)) return false;
     if (c->exploit != 0 && c->exploit != 1) return false;
+    if (c->refine != 0 && c->refine != 1) return false;
+    if (c->refine && (c->refine_period < 1 || c->refine_stride < 1 || c->refine_half < 0 ||
+                      c->refine_mature < 0 || c->refine_min_n < 1))
+        return false;
     if (c->exploit && (!std::isfinite(c->ph_delta) || !std::isfinite(c->ph_lambda) || c->ph_lambda < 0.0f ||
                        c->ph_window < 0 || c->ph_min_rounds < 0))
         return false;
@@ -1015,6 +1106,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     a.d = cfg->d;
     a.C = chunks_for(cfg->d);
     a.IW = inst_words(cfg->d);
+    a.stride0 = cfg->refine ? cfg->refine_stride : 1;
     a.inv_sqrt_lambda = (float)(1.0 / std::sqrt((double)cfg->lambda));
     const size_t work = (size_t)cfg->B * a.C * cfg->K;
     size_t blocks = (work + 255) / 256;
@@ -1055,6 +1147,10 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.e.lambda = c.ph_lambda;
     p.e.window = c.ph_window;
     p.e.min_rounds = c.ph_min_rounds;
+    p.rf.now = (c.refine && d_ctx != nullptr && h->t > 0 && h->t % c.refine_period == 0) ? 1 : 0;
+    p.rf.stat = h->t < c.refine_mature ? 1 : 0;
+    p.rf.half = c.refine_half;
+    p.rf.min_n = c.refine_min_n;
     p.hdr = at<StateHeader>(h->base, 0);
     p.ctx = d_ctx;
     p.reward = d_reward;

@@ -31,7 +31,8 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
                    a=torch.empty(T, P, dtype=torch.int32, device=dev),
                    mask=torch.empty(T, P, (wl.K + 31) // 32, dtype=torch.int32, device=dev),
                    kact=torch.empty(T, P, dtype=torch.int32, device=dev),
-                   ph=torch.empty(T, P, 9, dtype=torch.int32, device=dev))
+                   ph=torch.empty(T, P, 9, dtype=torch.int32, device=dev),
+                   win=torch.empty(T, P, 3, dtype=torch.int32, device=dev))
         if scores:
             rec["scores"] = torch.empty(T, P, 2, wl.K, device=dev)
         view = tuner.view()
@@ -45,6 +46,7 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
             rec["mask"][t] = view["mask"].index_select(0, pidx)
             rec["kact"][t] = view["kact"].index_select(0, pidx)
             rec["ph"][t] = view["ph"].index_select(0, pidx)
+            rec["win"][t] = view["window"].index_select(0, pidx)
             if scores:
                 rec["scores"][t] = sc.index_select(0, pidx)
         r, x = env.step(t, action)

@@ -20,7 +20,7 @@ class Tuner:
 
     def __init__(self, B, K, d, lam=1.0, alpha0=1.0, alpha_sched=0, prune_rule=0,
                  prune_period=50, device="cuda", stream=None, state=None, adopt=False,
-                 heuristics=None, exploit=None):
+                 heuristics=None, exploit=None, refine=None):
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
@@ -32,6 +32,10 @@ class Tuner:
         if exploit:
             self.cfg.exploit = 1
             for name, value in exploit.items():
+                setattr(self.cfg, name, value)
+        if refine:
+            self.cfg.refine = 1
+            for name, value in refine.items():
                 setattr(self.cfg, name, value)
         self.nbytes = L.agft_state_bytes(self.cfg)
         if self.nbytes == 0:
@@ -56,7 +60,8 @@ class Tuner:
     def from_workload(cls, wl, B=None, **kw):
         return cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0, wl.alpha_sched,
                    wl.prune, wl.period, heuristics=wl.heuristics(),
-                   exploit=wl.page_hinkley() if wl.exploit else None, **kw)
+                   exploit=wl.page_hinkley() if wl.exploit else None,
+                   refine=wl.refinement() if wl.refine else None, **kw)
 
     def close(self):
         if getattr(self, "h", None):
@@ -121,7 +126,7 @@ class Tuner:
             mask=region(v.mask, B * KW, torch.int32, (B, KW)),
             inst=inst,
             aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2], mode=inst[:, 3], ph=inst[:, 3:12],
-            xprev=inst[:, 12:12 + d].view(torch.float32),
+            window=inst[:, 12:15], xprev=inst[:, 16:16 + d].view(torch.float32),
             stats=region(v.stats, B * K * 2, torch.int32, (B, K, 2)),
             theta=region(v.theta, B * K * d, torch.float32, (B, K, d)) if v.theta else None,
         )

@@ -16,33 +16,32 @@ def say(*a):
 def run_open_loop(cfg, X, R, flush=True):
     """Drive a Tuner with given contexts X [T][B][d] and rewards R [T][B].
     Returns host arrays: actions [T][B], mask words [T][B][KW], scores
-    [T][B][2][K], the tuner, and (when cfg has exploit) the Page-Hinkley
-    words [T][B][9] after each step as a fifth item."""
+    [T][B][2][K], the tuner, and a dict of the Page-Hinkley words [T][B][9]
+    ("ph") and the action spaces [T][B][3] ("win") after each step."""
     T, B, d = X.shape
     dev = torch.device("cuda")
     tuner = Tuner(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
                   cfg["prune"], cfg["period"], device=dev, heuristics=cfg.get("heuristics"),
-                  exploit=cfg.get("exploit"))
+                  exploit=cfg.get("exploit"), refine=cfg.get("refine"))
     Xd = torch.as_tensor(np.asarray(X, dtype=np.float32), device=dev)
     Rd = torch.as_tensor(np.asarray(R, dtype=np.float32), device=dev)
     K, KW = cfg["K"], (cfg["K"] + 31) // 32
     acts = torch.empty(T, B, dtype=torch.int32, device=dev)
     masks = torch.empty(T, B, KW, dtype=torch.int32, device=dev)
     scores = torch.empty(T, B, 2, K, device=dev)
-    ph = torch.empty(T, B, 9, dtype=torch.int32, device=dev) if cfg.get("exploit") else None
+    ph = torch.empty(T, B, 9, dtype=torch.int32, device=dev)
+    win = torch.empty(T, B, 3, dtype=torch.int32, device=dev)
     view = tuner.view()
     for t in range(T):
         tuner.step(Xd[t], Rd[t - 1] if t > 0 else None, acts[t], scores[t])
         masks[t].copy_(view["mask"])
-        if ph is not None:
-            ph[t].copy_(view["ph"])
+        ph[t].copy_(view["ph"])
+        win[t].copy_(view["window"])
     if flush and T > 0:
         tuner.flush(Rd[T - 1])
     torch.cuda.synchronize()
-    out = (acts.cpu().numpy(), masks.cpu().numpy(), scores.cpu().numpy().astype(np.float64), tuner)
-    if ph is not None:
-        out += (ph.cpu().numpy(),)
-    return out
+    return (acts.cpu().numpy(), masks.cpu().numpy(), scores.cpu().numpy().astype(np.float64), tuner,
+            dict(ph=ph.cpu().numpy(), win=win.cpu().numpy()))
 
 
 def random_contexts(seed, T, B, d, scale=1.0):

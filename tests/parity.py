@@ -19,6 +19,11 @@ state is compared within PH_TOL, and an alarm that one side raised and the
 other did not is accepted only where the oracle's margin was within PH_TIE of
 zero; the oracle then adopts the GPU's test state (and, for that step, the
 GPU's decision, since the two scored in different modes).
+
+The refinement of the action space is compared after every committed step:
+the windows must be identical, except at a statistical refinement whose two
+candidate anchors have mean rewards within MEAN_TIE of each other (fp32 sums
+on the GPU, fp64 in the oracle); the oracle then adopts the GPU's window.
 """
 import numpy as np
 
@@ -30,6 +35,7 @@ TIE = 1e-5         # score gaps at or below this (times max(1, |score|)) are nea
 ENV_TOL = 1e-5     # contexts and rewards: fp32 environment vs fp64 environment
 PH_TOL = 1e-4      # Page-Hinkley statistics, closed loop (both fp32, rewards differ by rounding)
 PH_TIE = 1e-4      # |lambda - statistic| at or below this: the alarm could go either way
+MEAN_TIE = 1e-4    # mean rewards this close (relative): either can anchor a refinement
 
 
 def mask_words_to_bool(words, K):
@@ -44,18 +50,57 @@ class ParityError(AssertionError):
 
 class Checker:
     def __init__(self, name, K, ids, g_a, g_keep, g_s=None, g_x=None, g_r=None, rules=0,
-                 cascade_k=0, g_ph=None, strict_ph=False):
+                 cascade_k=0, g_ph=None, strict_ph=False, g_win=None, refine=None):
         self.name, self.K, self.ids = name, K, list(ids)
         self.g_a, self.g_keep, self.g_s, self.g_x, self.g_r = g_a, g_keep, g_s, g_x, g_r
         self.rules, self.cascade_k = rules, cascade_k
         # g_ph [T][n][9] int32: mode, Page-Hinkley n, mean, m+, min m+, m-, min m-,
         # last alarm round, last margin (fp32 bits), after each step
         self.g_ph, self.strict_ph = g_ph, strict_ph
+        # g_win [T][n][3] int32: action space lo, hi, stride after each step;
+        # refine: the refinement parameters (period, half, mature, min_n)
+        self.g_win, self.refine = g_win, refine
         self.oracle = None
         self.st = dict(max_score_err=0.0, max_ctx_err=0.0, max_reward_err=0.0, forced=0,
                        forced_prune=0, forced_rules=0, exact_tie_steps=0, decisions=0,
                        no_decision=0, max_ph_err=0.0, forced_ph=0, forced_mode=0,
-                       greedy_decisions=0)
+                       greedy_decisions=0, refinements=0, forced_window=0)
+
+    def _anchor(self, lo, hi):
+        h = self.refine["refine_half"]
+        if lo > 0:
+            return lo + h
+        if hi < self.K - 1:
+            return hi - h
+        return None
+
+    def after_commit(self, t):
+        """Compare the action spaces once step t is committed."""
+        if self.g_win is None:
+            return
+        rf = self.refine
+        for i in range(len(self.ids)):
+            o_win = tuple(self.oracle.window(i))
+            g_win = tuple(int(v) for v in self.g_win[t, i])
+            if t > 0 and t % rf["refine_period"] == 0 and g_win[2] == 1:
+                self.st["refinements"] += 1
+            if o_win == g_win:
+                continue
+            stat_step = t > 0 and t % rf["refine_period"] == 0 and t < rf["refine_mature"]
+            a_o, a_g = self._anchor(*o_win[:2]), self._anchor(*g_win[:2])
+            ok = stat_step and a_o is not None and a_g is not None and g_win[2] == 1
+            if ok:
+                st = self.oracle.get(i)
+                n, rs = st["nsel"], st["rsum"]
+                ok = n[a_g] >= rf["refine_min_n"] and n[a_o] >= rf["refine_min_n"]
+                if ok:
+                    m_o, m_g = rs[a_o] / n[a_o], rs[a_g] / n[a_g]
+                    ok = abs(m_o - m_g) <= MEAN_TIE * max(1.0, abs(m_o))
+            if not ok:
+                self.fail(f"action space differs after t={t}, instance {self.ids[i]}: GPU {g_win}, "
+                          f"oracle {o_win}")
+            self.oracle.set_window(i, *g_win)
+            self.st["forced_window"] += 1
 
     def bind(self, oracle):
         """The oracle whose Page-Hinkley state is checked (and forced)."""
@@ -204,20 +249,23 @@ def compare(wl, T, probes, rec):
                   rec["scores"].numpy().astype(np.float64) if "scores" in rec else None,
                   rec["x"].numpy().astype(np.float64), rec["r"].numpy().astype(np.float64),
                   rules=wl.prune, cascade_k=wl.cascade_k,
-                  g_ph=rec["ph"].numpy() if wl.exploit else None)
+                  g_ph=rec["ph"].numpy() if wl.exploit else None,
+                  g_win=rec["win"].numpy() if wl.refine else None,
+                  refine=wl.refinement() if wl.refine else None)
     out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14),
-                          on_create=chk.bind)
+                          on_create=chk.bind, on_commit=chk.after_commit)
     st = chk.finish()
     st["oracle"] = out["oracle"]
     return st
 
 
-def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None):
+def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None, g_win=None):
     """Open loop: contexts X [T][B][d] and rewards R [T][B] (reward of the
     decision at t) given to both sides.  cfg: dict(B, K, d, lam, alpha0,
-    sched, prune, period[, heuristics][, exploit]).  GPU records: actions
-    [T][B], mask words [T][B][KW] after each step, scores [T][B][2][K],
-    Page-Hinkley words [T][B][9] (when cfg has exploit)."""
+    sched, prune, period[, heuristics][, exploit][, refine]).  GPU records:
+    actions [T][B], mask words [T][B][KW] after each step, scores
+    [T][B][2][K], Page-Hinkley words [T][B][9] (when cfg has exploit), action
+    spaces [T][B][3] (when cfg has refine)."""
     T = X.shape[0]
     ora = Oracle(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
                  cfg["prune"], cfg["period"])
@@ -227,15 +275,20 @@ def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None):
     expl = cfg.get("exploit")
     if expl:
         ora.set_exploit(True, **expl)
+    ref = cfg.get("refine")
+    if ref:
+        ora.set_refine(True, **ref)
     chk = Checker(name, cfg["K"], range(cfg["B"]), g_a, mask_words_to_bool(g_masks, cfg["K"]), g_s,
                   rules=cfg["prune"], cascade_k=(heur or {}).get("cascade_k", 0),
-                  g_ph=g_ph if expl else None, strict_ph=True)
+                  g_ph=g_ph if expl else None, strict_ph=True,
+                  g_win=g_win if ref else None, refine=ref)
     chk.bind(ora)
     r_prev = None
     for t in range(T):
         ucb, lcb, keep, action, marg = ora.decide(X[t], r_prev, margins=True)
         a, k = chk(t, X[t], r_prev, ucb, lcb, keep, action, marg)
         ora.commit(X[t], a, k)
+        chk.after_commit(t)
         r_prev = R[t]
     ora.flush(r_prev)
     st = chk.finish()

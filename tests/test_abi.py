@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert L.agft_abi_version() == L.ABI_VERSION == 2
+    assert L.agft_abi_version() == L.ABI_VERSION == 3
     for code in (0, -1, -2, -3, -4):
         assert L.agft_strerror(code)
     assert L.agft_strerror(-99) == "unknown status"
@@ -67,7 +67,11 @@ def test_state_bytes(lib):
                 dict(prune_rule=4, hist_min_n=6, hist_min_arms=3, hist_kappa=-1.0),
                 dict(prune_rule=8, cascade_k=17),
                 dict(exploit=2), dict(exploit=1, ph_lambda=-1.0), dict(exploit=1, ph_delta=float("nan")),
-                dict(exploit=1, ph_window=-1), dict(exploit=1, ph_min_rounds=-5)):
+                dict(exploit=1, ph_window=-1), dict(exploit=1, ph_min_rounds=-5),
+                dict(refine=2), dict(refine=1, refine_period=0, refine_stride=10, refine_min_n=4),
+                dict(refine=1, refine_period=50, refine_stride=0, refine_min_n=4),
+                dict(refine=1, refine_period=50, refine_stride=10, refine_half=-1, refine_min_n=4),
+                dict(refine=1, refine_period=50, refine_stride=10, refine_min_n=0)):
         assert L.agft_state_bytes(_cfg(**bad)) == 0, bad
 
 

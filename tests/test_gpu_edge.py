@@ -22,7 +22,7 @@ def _cfg(B, K, d, lam=1.0, alpha0=0.5, sched=0, prune=0, period=50):
 def _open_loop_case(name, cfg, T, seed, scale=1.0):
     say(f"[edge] {name}: {cfg} T={T}")
     X, R = random_contexts(seed, T, cfg["B"], cfg["d"], scale)
-    a, m, s, tuner = run_open_loop(cfg, X, R)
+    a, m, s, tuner, _ = run_open_loop(cfg, X, R)
     st = parity.compare_open_loop(name, cfg, X, R, a, m, s)
     compare_model(tuner, st["oracle"], range(cfg["B"]), 1e-3, 1e-4)
     say(f"[edge] {name}: max score err {st['max_score_err']:.2e}, forced {st['forced']}/"
@@ -66,7 +66,7 @@ def test_untouched_arms_are_swept_in_order():
     X[:, :, 0] = 1.0
     X[:, :, 1:] = np.random.default_rng(5).standard_normal((1, B, d - 1)).astype(np.float32)
     R = -np.ones((K, B))
-    a, m, s, tuner = run_open_loop(cfg, X, R)
+    a, m, s, tuner, _ = run_open_loop(cfg, X, R)
     assert (a == np.arange(K)[:, None]).all()
 
 
@@ -102,7 +102,7 @@ def test_non_finite_inputs():
     X[12, 3, 4] = np.nan
     X[13, 3, 2] = np.inf
     X[20, 0, 0] = -np.inf
-    a, m, s, tuner = run_open_loop(cfg, X, R)
+    a, m, s, tuner, _ = run_open_loop(cfg, X, R)
     st = parity.compare_open_loop("non-finite", cfg, X, R, a, m, s)
     assert a[12, 3] == -1 and a[13, 3] == -1 and a[20, 0] == -1
     bad = tuner.view()["bad"].cpu().numpy()

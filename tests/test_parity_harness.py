@@ -25,7 +25,11 @@ def _record(cfg, X, R):
     T, B, _ = X.shape
     K = cfg["K"]
     ora = Oracle(B, K, cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"], cfg["prune"], cfg["period"])
-    ora.set_exploit(True, **cfg["exploit"])
+    if cfg.get("exploit"):
+        ora.set_exploit(True, **cfg["exploit"])
+    if cfg.get("refine"):
+        ora.set_refine(True, **cfg["refine"])
+    win = np.empty((T, B, 3), np.int32)
     KW = (K + 31) // 32
     acts = np.empty((T, B), np.int32)
     masks = np.zeros((T, B, KW), np.int64)
@@ -35,6 +39,7 @@ def _record(cfg, X, R):
     for t in range(T):
         ucb, lcb, keep, action = ora.decide(X[t], r_prev)
         ora.commit(X[t], action, keep)
+        win[t] = [ora.window(i) for i in range(B)]
         acts[t] = action
         for k in range(K):
             masks[t, :, k // 32] |= keep[:, k].astype(np.int64) << (k % 32)
@@ -46,7 +51,7 @@ def _record(cfg, X, R):
             ph[t, i, 7] = last
             ph[t, i, 8] = np.float32(margin).view(np.int32)
         r_prev = R[t]
-    return acts, masks.astype(np.uint32).view(np.int32), scores.astype(np.float32).astype(np.float64), ph
+    return acts, masks.astype(np.uint32).view(np.int32), scores.astype(np.float32).astype(np.float64), ph, win
 
 
 CFG = dict(B=6, K=12, d=8, lam=1.0, alpha0=0.5, sched=0, prune=1, period=20, exploit=FAST_PH)
@@ -54,7 +59,7 @@ CFG = dict(B=6, K=12, d=8, lam=1.0, alpha0=0.5, sched=0, prune=1, period=20, exp
 
 def test_oracle_record_passes():
     X, R = _inputs(3, 150, CFG["B"], CFG["d"])
-    a, m, s, ph = _record(CFG, X, R)
+    a, m, s, ph, _ = _record(CFG, X, R)
     assert (ph[-1, :, 0] >= 0).any() and (ph[:, :, 7] > 0).any()
     st = parity.compare_open_loop("self", CFG, X, R, a, m, s, g_ph=ph)
     assert st["greedy_decisions"] > 0 and st["forced_ph"] == 0
@@ -63,7 +68,7 @@ def test_oracle_record_passes():
 @pytest.mark.parametrize("plant", ["switch_round", "alarm_round", "statistic", "greedy_score"])
 def test_planted_difference_fails(plant):
     X, R = _inputs(3, 150, CFG["B"], CFG["d"])
-    a, m, s, ph = _record(CFG, X, R)
+    a, m, s, ph, _ = _record(CFG, X, R)
     modes = ph[-1, :, 0]
     i = int(np.flatnonzero(modes >= 0)[0])
     t_sw = int(modes[i])
@@ -79,3 +84,33 @@ def test_planted_difference_fails(plant):
         s[t_sw + 1, i, :, int(a[t_sw + 1, i])] += 1e-3
     with pytest.raises(parity.ParityError):
         parity.compare_open_loop("planted", CFG, X, R, a, m, s, g_ph=ph)
+
+
+RCFG = dict(B=4, K=30, d=4, lam=1.0, alpha0=0.5, sched=0, prune=1, period=13,
+            refine=dict(refine_period=6, refine_stride=5, refine_half=3, refine_mature=24,
+                        refine_min_n=2))
+
+
+def test_oracle_record_with_refinement_passes():
+    X, R = _inputs(8, 60, RCFG["B"], RCFG["d"])
+    a, m, s, _, win = _record(RCFG, X, R)
+    assert (win[:, :, 2] == 1).any()
+    st = parity.compare_open_loop("self-refine", RCFG, X, R, a, m, s, g_win=win)
+    assert st["refinements"] > 0 and st["forced_window"] == 0
+
+
+@pytest.mark.parametrize("plant", ["predictive_shift", "statistical_far_anchor", "stride"])
+def test_planted_window_difference_fails(plant):
+    X, R = _inputs(8, 60, RCFG["B"], RCFG["d"])
+    a, m, s, _, win = _record(RCFG, X, R)
+    if plant == "predictive_shift":            # one arm off after a predictive refinement
+        t = 30
+        win[t:, 0, :2] = np.minimum(win[t:, 0, :2] + 1, RCFG["K"] - 1)
+    elif plant == "statistical_far_anchor":    # a window around the arm with the worst mean
+        t = 6
+        win[t:, 1] = (0, 6, 1)
+    else:                                      # the coarse grid kept after a refinement
+        t = 12
+        win[t:, 2, 2] = RCFG["refine"]["refine_stride"]
+    with pytest.raises(parity.ParityError):
+        parity.compare_open_loop("planted-window", RCFG, X, R, a, m, s, g_win=win)
