@@ -336,10 +336,14 @@ void agft_step_kernel(StepArgs p) {
     __shared__ float s_red_v2[kMaxWaves];
     __shared__ int s_red_k2[kMaxWaves];
 
+    __shared__ float s_xp[D];   // context of the previous decision, for the update
+
     const bool decide = p.ctx != nullptr;
 
     // Per-instance words, uniform over the workgroup (scalar loads at kernel
-    // start): context, previous decision, its reward and its context.
+    // start): context, previous decision and its reward.  The previous
+    // decision's context is only needed by the update after the stream, so it
+    // waits in LDS rather than in scalar registers.
     float x[D];
     bool x_ok = decide;
     if (decide) {
@@ -359,12 +363,7 @@ void agft_step_kernel(StepArgs p) {
     const float r = has_prev ? p.reward[inst] : 0.0f;
     const bool upd = has_prev && isfinite(r);
     const int a_upd = upd ? a_prev : -1;
-    float xp[D];
-    if (upd) {
-        const float *xpi = reinterpret_cast<const float *>(blk + kInstX);
-#pragma unroll
-        for (int q = 0; q < D; ++q) xp[q] = xpi[q];
-    }
+    if (upd && wave == 0 && lane < D) s_xp[lane] = reinterpret_cast<const float *>(blk + kInstX)[lane];
 
     // Page-Hinkley test on the instance's rewards and the switch to greedy
     // exploitation (uniform scalar code, single precision, fixed order).
@@ -664,7 +663,7 @@ void agft_step_kernel(StepArgs p) {
             float fj = 0.0f;
 #pragma unroll
             for (int i = 0; i < D; ++i)
-                if (i <= lane) fj = fmaf(sS[packed(i, lane < D ? lane : 0)], xp[i], fj);
+                if (i <= lane) fj = fmaf(sS[packed(i, lane < D ? lane : 0)], s_xp[i], fj);
             if (lane >= D) fj = 0.0f;
             float incl = fj * fj;
 #pragma unroll
@@ -672,7 +671,7 @@ void agft_step_kernel(StepArgs p) {
                 const float y = __shfl_up(incl, off);
                 if (lane >= off) incl += y;
             }
-            float pred = lane < D ? pick<D>(xp, lane) * sth[lane < D ? lane : 0] : 0.0f;
+            float pred = lane < D ? s_xp[lane] * sth[lane] : 0.0f;
 #pragma unroll
             for (int off = kWave / 2; off > 0; off >>= 1) pred += __shfl_xor(pred, off);
             if (lane < D) {
