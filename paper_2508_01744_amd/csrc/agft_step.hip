@@ -405,7 +405,7 @@ void agft_step_kernel(StepArgs p) {
                                : tid == kInstPhMargin ? __float_as_int(ph_margin)
                                : __float_as_int(pick<6>(ph, tid - kInstPh));
 
-    // Record of the previous decision's arm: fetched now, consumed after the stream.
+    // Record of the previous decision's arm: fetched now, staged in LDS before the stream.
     float4 old_chunk[NQ];
     if (upd) {
         const float4 *src = recs + (size_t)a_upd * R::R;
@@ -570,6 +570,23 @@ void agft_step_kernel(StepArgs p) {
         xb[e] = (e > j && e >= 1) ? x[D - e < 0 ? 0 : D - e] : 0.0f;
     }
     const float xt0 = pick<D>(x, 2 * j), xt1 = pick<D>(x, 2 * j + 1);
+    // The previous decision's record, fetched at kernel start, goes to LDS in
+    // canonical order now, so that it holds no registers through the stream.
+    if (upd) {
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int c = tid + q * nthr;
+            if (c < R::R) {
+                const int sl = c / G, jj = c % G;
+                const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    const int ci = canon(D, jj, 4 * sl + qq);
+                    if (ci >= 0) s_old[ci] = v[qq];
+                }
+            }
+        }
+    }
     __syncthreads();
 
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
@@ -641,20 +658,6 @@ void agft_step_kernel(StepArgs p) {
 
     // ---- square-root rank-1 update of the previous decision's arm ----
     if (upd) {
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int c = tid + q * nthr;
-            if (c < R::R) {
-                const int sl = c / G, jj = c % G;
-                const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq) {
-                    const int ci = canon(D, jj, 4 * sl + qq);
-                    if (ci >= 0) s_old[ci] = v[qq];
-                }
-            }
-        }
-        __syncthreads();
         const float *sth = s_old;         // theta
         const float *sS = s_old + D;      // packed factor
         if (wave == 0) {
