@@ -181,11 +181,23 @@ __device__ __forceinline__ void slice_terms(const float *f, const float *xa, con
     w2 = fmaf(vb, vb, va * va);
 }
 
-// Sum over the G lanes of a group (butterfly: every lane ends with the total).
+// v of another lane of the same row, through a DPP lane pattern.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the G lanes of an aligned group (G = 2, 4, 8, 16), every lane
+// ending with the same total: pairs within quads, then the two pairs of a
+// quad, then mirrored half rows (8 lanes) and mirrored rows (16 lanes), each
+// step a DPP add on the vector unit.
 template <int G>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    static_assert(G == 1 || G == 2 || G == 4 || G == 8 || G == 16, "group of 1..16 lanes");
+    if constexpr (G >= 2) v += dpp<0xB1>(v);    // quad_perm [1,0,3,2]
+    if constexpr (G >= 4) v += dpp<0x4E>(v);    // quad_perm [2,3,0,1]
+    if constexpr (G >= 8) v += dpp<0x141>(v);   // row_half_mirror
+    if constexpr (G >= 16) v += dpp<0x140>(v);  // row_mirror
     return v;
 }
 
@@ -614,45 +626,48 @@ void agft_step_kernel(StepArgs p) {
             }
         }
     } else {
-        float4 cur[S], nxt[S];
-        int k_cur = grp < nlist ? s_list[grp] : -1;
-        if (k_cur >= 0) {
-            const float4 *src = recs + (size_t)k_cur * R::R + j;
+        // two buffers of S chunks per lane, used in turn: one pass is
+        // scored while the next one's loads are in flight
+        float4 buf_a[S], buf_b[S];
+        auto fetch = [&](int k, float4 *dst) {
+            const float4 *src = recs + (size_t)k * R::R + j;
 #pragma unroll
-            for (int sidx = 0; sidx < S; ++sidx) cur[sidx] = ld_nt(src + sidx * G);
-        }
-        for (int base = 0; base < nlist; base += apw) {
-            const int slot_n = base + apw + grp;
-            const int k_nxt = slot_n < nlist ? s_list[slot_n] : -1;
-            if (k_nxt >= 0) {
-                const float4 *src = recs + (size_t)k_nxt * R::R + j;
-#pragma unroll
-                for (int sidx = 0; sidx < S; ++sidx) nxt[sidx] = ld_nt(src + sidx * G);
-            }
+            for (int sidx = 0; sidx < S; ++sidx) dst[sidx] = ld_nt(src + sidx * G);
+        };
+        auto score = [&](const float4 *c4, int k) {
             float f[4 * S];
 #pragma unroll
             for (int sidx = 0; sidx < S; ++sidx) {
-                f[4 * sidx + 0] = cur[sidx].x;
-                f[4 * sidx + 1] = cur[sidx].y;
-                f[4 * sidx + 2] = cur[sidx].z;
-                f[4 * sidx + 3] = cur[sidx].w;
+                f[4 * sidx + 0] = c4[sidx].x;
+                f[4 * sidx + 1] = c4[sidx].y;
+                f[4 * sidx + 2] = c4[sidx].z;
+                f[4 * sidx + 3] = c4[sidx].w;
             }
             float m, w2;
             slice_terms<D>(f, xa, xb, xt0, xt1, m, w2);
-            if (k_cur < 0) {
+            if (k < 0) {
                 m = 0.0f;
                 w2 = 0.0f;
             }
             m = group_sum<G>(m);
             w2 = group_sum<G>(w2);
-            if (k_cur >= 0 && j == 0) {
+            if (k >= 0 && j == 0) {
                 const float w = sqrtf(w2);
-                s_ucb[k_cur] = fmaf(p.alpha, w, m);
-                s_lcb[k_cur] = fmaf(-p.alpha, w, m);
+                s_ucb[k] = fmaf(p.alpha, w, m);
+                s_lcb[k] = fmaf(-p.alpha, w, m);
             }
-#pragma unroll
-            for (int sidx = 0; sidx < S; ++sidx) cur[sidx] = nxt[sidx];
-            k_cur = k_nxt;
+        };
+        auto list_at = [&](int slot) { return slot < nlist ? (int)s_list[slot] : -1; };
+        int k_a = list_at(grp);
+        if (k_a >= 0) fetch(k_a, buf_a);
+        for (int base = 0; base < nlist; base += 2 * apw) {
+            const int k_b = list_at(base + apw + grp);
+            if (k_b >= 0) fetch(k_b, buf_b);
+            score(buf_a, k_a);
+            if (base + apw >= nlist) break;
+            k_a = list_at(base + 2 * apw + grp);
+            if (k_a >= 0) fetch(k_a, buf_a);
+            score(buf_b, k_b);
         }
     }
 
