@@ -48,6 +48,7 @@
 #include <cstdint>
 #include <cstring>
 #include <new>
+#include <type_traits>
 
 #include "agft.h"
 
@@ -289,10 +290,64 @@ __device__ inline BestPair better(BestPair a, BestPair b) {
     return a;
 }
 
+// Partner value for step s (0..5) of a 64-lane butterfly: quad pairs, quads,
+// mirrored half rows, mirrored rows (all DPP, within rows of 16 lanes), then
+// rows 16 and 32 lanes apart.  After the six steps of an associative and
+// commutative op every lane holds the same result.
+template <int STEP>
+__device__ __forceinline__ int partner(int v) {
+    if constexpr (STEP == 0) return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+    else if constexpr (STEP == 1) return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+    else if constexpr (STEP == 2) return __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+    else if constexpr (STEP == 3) return __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false);
+    else if constexpr (STEP == 4) return __shfl_xor(v, 16);
+    else return __shfl_xor(v, 32);
+}
+template <int STEP>
+__device__ __forceinline__ float partner(float v) { return __int_as_float(partner<STEP>(__float_as_int(v))); }
+
+template <class T, class Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op) {
+    v = op(v, partner<0>(v));
+    v = op(v, partner<1>(v));
+    v = op(v, partner<2>(v));
+    v = op(v, partner<3>(v));
+    v = op(v, partner<4>(v));
+    return op(v, partner<5>(v));
+}
+
+__device__ __forceinline__ BestPair wave_best(BestPair b) {
+    auto step = [&](BestPair o) { b = better(b, o); };
+    step(BestPair{partner<0>(b.v), partner<0>(b.k)});
+    step(BestPair{partner<1>(b.v), partner<1>(b.k)});
+    step(BestPair{partner<2>(b.v), partner<2>(b.k)});
+    step(BestPair{partner<3>(b.v), partner<3>(b.k)});
+    step(BestPair{partner<4>(b.v), partner<4>(b.k)});
+    step(BestPair{partner<5>(b.v), partner<5>(b.k)});
+    return b;
+}
+
+// Inclusive prefix sum over lanes 0..31 (DPP shifts within rows of 16, then
+// the first row's total added to the second row); lanes 32..63 unspecified.
+template <class T>
+__device__ __forceinline__ T scan32(T v) {
+    auto shr = [](T x, auto ctrl) {
+        const int xi = __builtin_bit_cast(int, x);
+        return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(0, xi, decltype(ctrl)::value, 0xF, 0xF, true));
+    };
+    v += shr(v, std::integral_constant<int, 0x111>{});   // row_shr:1
+    v += shr(v, std::integral_constant<int, 0x112>{});   // row_shr:2
+    v += shr(v, std::integral_constant<int, 0x114>{});   // row_shr:4
+    v += shr(v, std::integral_constant<int, 0x118>{});   // row_shr:8
+    const int vi = __builtin_bit_cast(int, v);
+    v += __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(0, vi, 0x142, 0xA, 0xF, false));  // row_bcast:15
+    return v;
+}
+
 // Workgroup-wide reductions through one LDS slot per wavefront.
 template <class T, class Op>
 __device__ T block_reduce(T v, T *red, int lane, int wave, int nwave, Op op) {
-    for (int off = kWave / 2; off > 0; off >>= 1) v = op(v, __shfl_xor(v, off));
+    v = wave_reduce(v, op);
     if (lane == 0) red[wave] = v;
     __syncthreads();
     T out = red[0];
@@ -517,12 +572,8 @@ void agft_step_kernel(StepArgs p) {
                     first = k < first ? k : first;
                     if (__float_as_int(s_ucb[k]) > 0) bk = better(bk, BestPair{s_lcb[k], k});
                 }
-            for (int off = kWave / 2; off > 0; off >>= 1) {
-                BestPair o{__shfl_xor(bk.v, off), __shfl_xor(bk.k, off)};
-                bk = better(bk, o);
-                const int of = __shfl_xor(first, off);
-                first = of < first ? of : first;
-            }
+            bk = wave_best(bk);
+            first = wave_reduce(first, [](int a, int b) { return a < b ? a : b; });
             if (lane == 0) {
                 s_red_v[wave] = bk.v;
                 s_red_k[wave] = bk.k;
@@ -559,12 +610,7 @@ void agft_step_kernel(StepArgs p) {
         if (x_ok && a_upd >= 0 && (a_upd >> 5) == lane) wl &= ~(1u << (a_upd & 31));
         if (!x_ok) wl = 0u;
         const int cnt = __popc(wl);
-        int incl = cnt;
-#pragma unroll
-        for (int off = 1; off < kMaxWords; off <<= 1) {
-            const int y = __shfl_up(incl, off);
-            if (lane >= off) incl += y;
-        }
+        const int incl = scan32(cnt);
         int pos = incl - cnt;
         while (wl) {
             const int b = __ffs(wl) - 1;
@@ -683,15 +729,9 @@ void agft_step_kernel(StepArgs p) {
             for (int i = 0; i < D; ++i)
                 if (i <= lane) fj = fmaf(sS[packed(i, lane < D ? lane : 0)], s_xp[i], fj);
             if (lane >= D) fj = 0.0f;
-            float incl = fj * fj;
-#pragma unroll
-            for (int off = 1; off < D; off <<= 1) {
-                const float y = __shfl_up(incl, off);
-                if (lane >= off) incl += y;
-            }
+            const float incl = scan32(fj * fj);
             float pred = lane < D ? s_xp[lane] * sth[lane] : 0.0f;
-#pragma unroll
-            for (int off = kWave / 2; off > 0; off >>= 1) pred += __shfl_xor(pred, off);
+            pred = wave_reduce(pred, [](float a, float b) { return a + b; });
             if (lane < D) {
                 const float al = 1.0f + incl;
                 const float al_prev = 1.0f + (incl - fj * fj);
@@ -800,7 +840,7 @@ void agft_step_kernel(StepArgs p) {
         float l = -INFINITY;
         for (int k = tid; k < K; k += nthr)
             if (is_active(k)) l = fmaxf(l, s_lcb[k]);
-        for (int off = kWave / 2; off > 0; off >>= 1) l = fmaxf(l, __shfl_xor(l, off));
+        l = wave_reduce(l, [](float a, float b) { return fmaxf(a, b); });
         if (lane == 0) s_red_v[wave] = l;
         __syncthreads();
         for (int w = 0; w < nwave; ++w) lstar = fmaxf(lstar, s_red_v[w]);
@@ -845,12 +885,9 @@ void agft_step_kernel(StepArgs p) {
             }
         }
     }
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        BestPair o{__shfl_xor(b.v, off), __shfl_xor(b.k, off)};
-        b = better(b, o);
-        n += __shfl_xor(n, off);
-        if (stat_anchor) sb = better(sb, BestPair{__shfl_xor(sb.v, off), __shfl_xor(sb.k, off)});
-    }
+    b = wave_best(b);
+    n = wave_reduce(n, [](int a, int c) { return a + c; });
+    if (stat_anchor) sb = wave_best(sb);
     if (lane == 0) {
         s_red_v[wave] = b.v;
         s_red_k[wave] = b.k;
@@ -886,7 +923,7 @@ void agft_step_kernel(StepArgs p) {
         if (anchor >= 0) {
             // arms in play in the new space
             int c2 = lane < KW ? __popc(s_raw[lane] & space_bits(lane, nlo, nhi, 1)) : 0;
-            for (int off = kWave / 2; off > 0; off >>= 1) c2 += __shfl_xor(c2, off);
+            c2 = wave_reduce(c2, [](int a, int c) { return a + c; });
             cnt = c2;
         }
         if (lane == 0) {
