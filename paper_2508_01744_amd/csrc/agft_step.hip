@@ -145,25 +145,29 @@ Layout layout_for(int B, int K, int d, int exploit) {
 // Dynamic LDS of the step kernel: UCB and LCB per arm, then the arm list.
 size_t step_lds_bytes(int K) { return ((size_t)K * (2 * 4 + 2) + 15) / 16 * 16; }
 
-// Workgroup width (wavefronts) for K arms of dimension d; one workgroup per
-// instance, looping over the arms in passes of 64*w/(d/2).  The step is a
-// chain of dependent phases per instance, so narrow workgroups (more
-// instances in flight per CU, cheaper barriers) win unless each instance
-// streams many whole records:
-//   1 when one wavefront covers the arms in at most 8 passes;
-//   2 at d = 32 (3 wavefronts per SIMD fit its registers, so 2-wave groups
-//     keep twice as many instances resident as 4-wave ones);
-//   1 when the switch to exploitation is on (exploiting instances read d
-//     floats per arm);
-//   4 otherwise.
-// Measured on MI355X (step kernel, us): K=64 d=8 B=4096: 21 / 25 / 30 for
-// w = 1 / 2 / 4; K=256 d=32 B=1024: 34 / 31 / 40; K=128 d=16 B=65536: 895 /
-// 892 / 882; the same with the switch on: 595 / 602 / 672.
-int waves_for(int K, int d, int exploit) {
-    const int lanes = K * (d / 2);
-    if (lanes <= 8 * kWave) return 1;
-    if (d == 32) return 2;
-    return exploit ? 1 : 4;
+// Workgroup width (wavefronts); one workgroup per instance, looping over its
+// arms in passes of 64*w/(d/2).  The step is a chain of dependent phases per
+// instance, so narrow workgroups (more instances in flight per CU, cheaper
+// barriers) win unless each instance streams many bytes.  The bytes per
+// step are estimated from the arms in play (with the refinement, at most the
+// larger of the coarse grid and the window) times what each costs (the
+// record, or the theta copy once instances exploit): one wavefront up to
+// 16 KB, four beyond.  Measured on MI355X (step kernel, us, w = 1 / 2 / 4):
+//   K=64 d=8 B=4,096 (12 KB):              21 / 25 / 30
+//   K=128 d=16 B=65,536 (80 KB):           895 / 892 / 882
+//   the same, exploitation (8 KB):         595 / 602 / 672
+//   the same, refinement (13 KB):          190 / 231 / 376
+//   K=256 d=32 B=1,024 (590 KB):           31 / 29 / 29
+//   the same, exploitation (32 KB):        43 / 34 / 31
+int waves_for(const agft_config &c) {
+    int k_eff = c.K;
+    if (c.refine) {
+        const int coarse = (c.K - 1) / c.refine_stride + 1, window = 2 * c.refine_half + 1;
+        k_eff = coarse > window ? coarse : window;
+        if (k_eff > c.K) k_eff = c.K;
+    }
+    const size_t per_arm = c.exploit ? 4 * (size_t)c.d : 16 * (size_t)chunks_for(c.d);
+    return (size_t)k_eff * per_arm <= 16384 ? 1 : 4;
 }
 
 // Per-lane slice of the Eq. 1 terms from the S chunks of one record slice:
@@ -359,7 +363,7 @@ __device__ T block_reduce(T v, T *red, int lane, int wave, int nwave, Op op) {
 // Wavefronts per SIMD the register allocation must allow, by context dimension.
 template <int D>
 struct Occupancy {
-    static constexpr int waves = D == 32 ? 3 : 7;
+    static constexpr int waves = D == 32 ? 4 : 7;
 };
 
 template <int D>
@@ -1219,7 +1223,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
-    const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves_for(c.K, c.d, c.exploit)));
+    const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves_for(c)));
     const size_t lds = step_lds_bytes(c.K);
     switch (c.d) {
         case 8: hipLaunchKernelGGL(agft_step_kernel<8>, grid, block, lds, h->stream, p); break;
