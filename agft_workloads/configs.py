@@ -34,7 +34,7 @@ class Workload:
     drift: float = 0.0   # power/latency coefficients b, c scale to (1 + drift) at t = T - 1
     description: str = ""
     # the paper's pruning heuristics (rule bits 2, 4, 8; Sec. 4.3): the example
-    # values the paper gives, plus this build's reading of the unstated ones
+    # values the paper gives, plus a reading of the unstated ones
     # (tolerance multiplier and the minimum number of compared arms)
     ext_rounds: int = 60
     ext_min_n: int = 3

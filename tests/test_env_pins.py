@@ -1,6 +1,6 @@
 """The fp64 environment model against closed forms and invariants (CPU only).
 
-The environment's constants are this build's own (the paper prints no worked
+The environment's constants are chosen here (the paper prints no worked
 example of its reward or features), so only its structure is pinned here:
 the energy-delay product's defining identities and the position of its
 optimum, the integer service capacities, and the context layout.
