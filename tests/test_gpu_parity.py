@@ -57,7 +57,7 @@ def test_small_paper_pruning(cfg):
     _run_and_compare(wl, list(range(wl.B)))
 
 
-@pytest.mark.parametrize("cfg", ["cfg2p", "cfg4p"])
+@pytest.mark.parametrize("cfg", ["cfg2p", "cfg3p", "cfg4p", "cfg5p"])
 def test_full_size_paper_pruning(cfg):
     wl = get_workload(cfg)
     _run_and_compare(wl, probe_instances(wl.B, 64))

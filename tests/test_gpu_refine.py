@@ -85,7 +85,7 @@ def test_small_closed_loop(name):
     _closed(wl, list(range(wl.B)))
 
 
-@pytest.mark.parametrize("name", ["cfg4r", "cfg4per"])
+@pytest.mark.parametrize("name", ["cfg2r", "cfg3r", "cfg4r", "cfg5r", "cfg4per"])
 def test_full_size_closed_loop(name):
     wl = get_workload(name)
     _closed(wl, probe_instances(wl.B, 64))
