@@ -133,3 +133,13 @@ def test_env_validation(lib):
     assert L.agft_env_step(cfg, p, n, -1, p, p, p, p, p, None) == L.AGFT_E_INVAL
     assert L.agft_env_step(cfg, p, n, cfg.T, p, p, p, p, p, None) == L.AGFT_E_INVAL
     assert L.agft_env_step(cfg, p, n, 0, None, p, p, p, p, None) == L.AGFT_E_INVAL
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """No silent fallback: without the built library every entry point raises."""
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "libagft.so"))
+    monkeypatch.setattr(L, "_lib", None)
+    with pytest.raises(RuntimeError, match="missing"):
+        L.lib()
+    with pytest.raises(RuntimeError):
+        L.agft_abi_version()

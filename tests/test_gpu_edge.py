@@ -188,3 +188,37 @@ def test_paper_pruning_rules(d, K, rules):
     kact = tuner.view()["kact"].cpu().numpy()
     assert (kact >= 1).all() and (kact < K).any()
     say(f"[edge] rules forced {st['forced_rules']}")
+
+
+def test_side_stream_and_stream_switch():
+    """The same closed-loop run enqueued on a side stream (default priority),
+    moved back to the default stream halfway, ends in a bit-identical state."""
+    from paper_2508_01744_amd import GpuEnv, env_config
+    wl = get_workload(3, B=32, T=120)
+    arr, noi = exogenous(wl)
+    ref = run_closed_loop(wl, ENV, arr, noi, probes=range(wl.B))
+    dev = torch.device("cuda")
+    main = torch.cuda.current_stream(dev)
+    side = torch.cuda.Stream(device=dev)
+    side.wait_stream(main)
+    with torch.cuda.stream(side):
+        arr_d, noi_d = torch.as_tensor(arr, device=dev), torch.as_tensor(noi, device=dev)
+        env = GpuEnv(env_config(wl, ENV), arr_d, noi_d, stream=side)
+        tun = Tuner.from_workload(wl, device=dev, stream=side)
+        act = torch.empty(wl.B, dtype=torch.int32, device=dev)
+        x, r, acts = env.reset(), None, []
+        for t in range(60):
+            tun.step(x, r, act)
+            acts.append(act.clone())
+            r, x = env.step(t, act)
+    main.wait_stream(side)
+    tun.set_stream(main)
+    env.stream = main
+    for t in range(60, wl.T):
+        tun.step(x, r, act)
+        acts.append(act.clone())
+        r, x = env.step(t, act)
+    tun.flush(r)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.stack(acts).cpu(), ref["probes"]["a"])
+    assert torch.equal(tun.state, ref["tuner"].state)
