@@ -30,6 +30,11 @@ of arm k (svc_init for the warm-up window).  The context of decision t is
 with z_w, rho_w the features and reward of window w, and windows before 0
 repeating window 0.  The reward of decision t is rho_{t+1}.  An action of -1
 (no decision) keeps the previous clock.
+
+The paper prints no worked example of its reward or features, so the
+constants (agft_workloads.ENV) are parity unpinned with respect to it; the
+tests pin this model's structure instead (the EDP identities, the position of
+its optimum, the integer capacities, the context layout).
 """
 import numpy as np
 
