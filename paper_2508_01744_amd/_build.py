@@ -29,5 +29,23 @@ def build(verbose=False, extra_flags=()):
     return LIB
 
 
+C_EXAMPLE_SRC = os.path.join(ROOT, "tests", "c_abi", "agft_c_example.c")
+C_EXAMPLE = os.path.join(ROOT, "tests", "c_abi", "agft_c_example")
+
+
+def build_c_example(verbose=False):
+    """Compile the plain C caller of the ABI (host code, gcc) against libagft.so."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE,
+           "-I", os.path.join(rocm, "include"), C_EXAMPLE_SRC, "-L", PKG, "-lagft",
+           "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/../../paper_2508_01744_amd", "-Wl,-rpath," + os.path.join(rocm, "lib"),
+           "-o", C_EXAMPLE]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return C_EXAMPLE
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
