@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define AGFT_ABI_VERSION 3
+#define AGFT_ABI_VERSION 4
 
 enum agft_status {
     AGFT_OK = 0,
@@ -135,17 +135,28 @@ typedef struct agft_state_view {
     int64_t t;          /* decisions made so far */
     int32_t pending;    /* 1 while the last decision awaits its reward */
     int32_t B, K, d;
-    int32_t chunks;     /* float4 chunks per arm record: (d/2) * ((d+6)/4) */
+    int32_t chunks;     /* float4 chunks per arm record: (d/2)*(d/4) + (d/2)*TF/4 */
+    int32_t block_arms; /* arms per block of records: NB = 64/d */
+    int32_t tail_floats;/* TF, floats per lane slice of a record tail: 3 (packed, no
+                           padding) when an exploring instance streams more than
+                           16 KB of records per step (arms in play * 4 * (d +
+                           d(d+1)/2) bytes), else 4 (one float of padding per slice,
+                           so that no tail straddles two 128-byte lines) */
     int32_t mask_words; /* uint32 words per instance in the action-set mask: ceil(K/32) */
-    void *arms;         /* float4 [B][K][chunks]: arm k of instance i is the contiguous
-                           record at index (i*K + k)*chunks.  A record is split into
-                           G = d/2 lane slices of (d+6)/4 chunks; chunk s*G + j holds
-                           positions 4s..4s+3 of slice j, whose positions are
+    void *arms;         /* float4 records, instance i's at chunk i * ceil(K/NB)*NB*chunks.
+                           Arm k sits in block k/NB (NB*chunks chunks), slot r = k%NB.
+                           A block holds the NB main parts (M = (d/2)*(d/4) chunks each,
+                           slot r at chunk r*M), then the NB tails (T = (d/2)*TF/4
+                           chunks each, slot r at chunk NB*M + r*T).  Every record has
+                           G = d/2 lane slices of d+3 positions:
                              e = 0..j:      S_{e,j}            (column j of S)
                              e = j+1..d:    S_{d-e, d-1-j}     (column d-1-j, bottom up)
                              e = d+1, d+2:  theta_{2j}, theta_{2j+1}
-                             e > d+2:       0
-                           with S upper triangular, S S^T = A^{-1}. */
+                           with S upper triangular, S S^T = A^{-1}.  Positions e < d of
+                           slice j are component e%4 of main chunk (e/4)*G + j;
+                           positions d..d+2 are tail floats TF*j .. TF*j+2 (with
+                           TF = 4, float TF*j+3 is 0).  Slots past K in the last
+                           block hold zeros. */
     uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k not
                            removed by a pruning rule (the action space is apart) */
     int32_t *inst;      /* [B][inst_words] per-instance block of 32-bit words:

@@ -36,7 +36,8 @@ class agft_config(ctypes.Structure):
 
 class agft_state_view(ctypes.Structure):
     _fields_ = [("t", _i64), ("pending", _i32), ("B", _i32), ("K", _i32), ("d", _i32),
-                ("chunks", _i32), ("mask_words", _i32), ("arms", _vp), ("mask", _vp),
+                ("chunks", _i32), ("block_arms", _i32), ("tail_floats", _i32),
+                ("mask_words", _i32), ("arms", _vp), ("mask", _vp),
                 ("inst", _vp), ("inst_words", _i32), ("stats", _vp), ("theta", _vp)]
 
 
@@ -50,7 +51,7 @@ class agft_env_config(ctypes.Structure):
                 ("mu", _f32 * 7), ("sd", _f32 * 7)]
 
 
-ABI_VERSION = 3   # AGFT_ABI_VERSION of the agft_config layout declared here
+ABI_VERSION = 4   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
             "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version",

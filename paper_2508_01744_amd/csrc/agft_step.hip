@@ -70,25 +70,45 @@ struct alignas(16) StateHeader {
     float lambda, alpha0;
     int32_t alpha_sched, prune_rule, prune_period;
     int32_t exploit;      // 1: the buffer holds the theta copy of the switch
-    uint32_t reserved[46];
+    int32_t tail_floats;  // record layout: floats per lane slice of a tail
+    uint32_t reserved[45];
 };
 static_assert(sizeof(StateHeader) == 256, "header is 256 bytes");
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 // Record geometry for context dimension D: G lanes per arm, each owning
-// P = D + 1 factor elements and two theta entries, padded to S float4 chunks.
-template <int D>
+// D + 3 positions (D + 1 factor elements and two theta entries).  Positions
+// 0..D-1 of every lane form the arm's main part (D/4 float4 chunks per
+// lane, lane-interleaved); positions D..D+2 its tail, TF floats per lane.
+// NB = 64/D arms make a block: their main parts, then their tails, so that
+// every main part starts on a 128-byte line.  With TF = 3 records carry no
+// padding (608 bytes at D = 16) and the NB tails fill three whole lines,
+// but half of them straddle two; with TF = 4 each tail slice is padded to
+// a chunk and every tail sits in one line.  An instance's arms take
+// ceil(K/NB) blocks.
+template <int D, int TF>
 struct Rec {
     static constexpr int G = D / 2;              // lanes per arm
     static constexpr int P = D + 1;              // factor elements per lane
-    static constexpr int S = (D + 3 + 3) / 4;    // chunks per lane
-    static constexpr int R = G * S;              // chunks per record
+    static constexpr int MQ = D / 4;             // main chunks per lane
+    static constexpr int S = MQ + 1;             // register slots per lane (the last holds the tail)
+    static constexpr int MAIN = G * MQ;          // main chunks per arm
+    static constexpr int TAIL = G * TF / 4;      // tail chunks per arm
+    static constexpr int R = MAIN + TAIL;        // chunks per record
+    static constexpr int NB = 32 / G;            // arms per block
+    static constexpr int BLK = NB * R;           // chunks per block
     static constexpr int NSE = D * (D + 1) / 2;  // packed factor elements
     static constexpr int CAN = D + NSE;          // canonical floats: theta, then packed S
 };
 
-int chunks_for(int d) { return (d / 2) * ((d + 6) / 4); }
+int chunks_for(int d, int tf) { return (d / 2) * (d / 4) + (d / 2) * tf / 4; }
+int block_arms(int d) { return 64 / d; }
+// float4 chunks of one instance's arm records: whole blocks
+size_t instance_chunks(int K, int d, int tf) {
+    const int nb = block_arms(d);
+    return (size_t)((K + nb - 1) / nb) * nb * chunks_for(d, tf);
+}
 
 // Packed column-major index of S_ij (i <= j) within the factor part.
 __host__ __device__ constexpr int packed(int i, int j) { return j * (j + 1) / 2 + i; }
@@ -101,6 +121,23 @@ __host__ __device__ constexpr int canon(int D, int j, int e) {
          : e == D + 1 ? 2 * j
          : e == D + 2 ? 2 * j + 1
          : -1;
+}
+
+// Chunk c of arm k's record, as an offset (in chunks) from the instance's
+// first block: chunks 0..MAIN-1 are the main part, the rest the tail.
+__host__ __device__ constexpr size_t rec_chunk(int D, int TF, int k, int c) {
+    const int G = D / 2, NB = 64 / D, MAIN = G * (D / 4), TAIL = G * TF / 4;
+    const size_t blk = (size_t)(k / NB) * NB * (MAIN + TAIL);
+    return c < MAIN ? blk + (size_t)(k % NB) * MAIN + c
+                    : blk + (size_t)NB * MAIN + (size_t)(k % NB) * TAIL + (c - MAIN);
+}
+
+// Canonical index of component q of record chunk c; -1 for padding.
+__host__ __device__ constexpr int canon_chunk(int D, int TF, int c, int q) {
+    const int G = D / 2, MAIN = G * (D / 4);
+    if (c < MAIN) return canon(D, c % G, 4 * (c / G) + q);
+    const int t = 4 * (c - MAIN) + q;   // tail float: lane t/TF, position D + t%TF
+    return t % TF < 3 ? canon(D, t / TF, D + t % TF) : -1;
 }
 
 // Column j and row i of packed element e.
@@ -127,24 +164,6 @@ struct Layout {
     size_t arms, mask, inst, stats, theta, total;
 };
 
-// theta copy [B][K][d] only with the switch to exploitation (0 bytes otherwise)
-Layout layout_for(int B, int K, int d, int exploit) {
-    Layout L;
-    const size_t b = (size_t)B, k = (size_t)K;
-    const size_t kw = (k + 31) / 32;
-    size_t off = sizeof(StateHeader);
-    L.arms = off;  off = align_up(off + b * k * (size_t)chunks_for(d) * 16);
-    L.mask = off;  off = align_up(off + b * kw * 4);
-    L.inst = off;  off = align_up(off + b * (size_t)inst_words(d) * 4);
-    L.stats = off; off = align_up(off + b * k * 8);
-    L.theta = off; off = align_up(off + (exploit ? b * k * (size_t)d * 4 : 0));
-    L.total = off;
-    return L;
-}
-
-// Dynamic LDS of the step kernel: UCB and LCB per arm, then the arm list.
-size_t step_lds_bytes(int K) { return ((size_t)K * (2 * 4 + 2) + 15) / 16 * 16; }
-
 // Arms an instance may have in play: K, or with the refinement the larger of
 // the coarse grid and the window.
 int arms_in_play(const agft_config &c) {
@@ -154,8 +173,41 @@ int arms_in_play(const agft_config &c) {
     return k < c.K ? k : c.K;
 }
 
-// Bytes an exploring instance streams per step, at most.
-size_t explore_bytes(const agft_config &c) { return (size_t)arms_in_play(c) * 16 * chunks_for(c.d); }
+// Bytes an exploring instance streams per step, at most: theta and the
+// packed factor of every arm in play.
+size_t explore_bytes(const agft_config &c) {
+    return (size_t)arms_in_play(c) * 4 * (size_t)(c.d + c.d * (c.d + 1) / 2);
+}
+
+// Record layout: packed tails (TF = 3) where an exploring instance streams
+// more than 16 KB per step, so that the stream moves no padding; padded
+// tails (TF = 4) otherwise, where the update's one-record read and
+// write-back weigh more than the stream and a tail that straddles two
+// lines costs more than its padding.  Measured on MI355X (step kernel,
+// packed / padded tails): K=128 d=16 B=65,536 (76 KB) 853 / 889 us, the
+// same with exploitation 827 / 845 us, K=256 d=32 B=1,024 (560 KB) 92.0 /
+// 93.0 us; K=64 d=8 B=4,096 (11 KB) 18.8 / 18.3 us, K=128 d=16 B=65,536
+// with the refinement (13 KB) 186 / 176 us, with the refinement, the rules
+// and the switch 190 / 179 us.
+int tail_floats(const agft_config &c) { return explore_bytes(c) > 16384 ? 3 : 4; }
+
+// theta copy [B][K][d] only with the switch to exploitation (0 bytes otherwise)
+Layout layout_for(const agft_config &c) {
+    Layout L;
+    const size_t b = (size_t)c.B, k = (size_t)c.K;
+    const size_t kw = (k + 31) / 32;
+    size_t off = sizeof(StateHeader);
+    L.arms = off;  off = align_up(off + b * instance_chunks(c.K, c.d, tail_floats(c)) * 16);
+    L.mask = off;  off = align_up(off + b * kw * 4);
+    L.inst = off;  off = align_up(off + b * (size_t)inst_words(c.d) * 4);
+    L.stats = off; off = align_up(off + b * k * 8);
+    L.theta = off; off = align_up(off + (c.exploit ? b * k * (size_t)c.d * 4 : 0));
+    L.total = off;
+    return L;
+}
+
+// Dynamic LDS of the step kernel: UCB and LCB per arm, then the arm list.
+size_t step_lds_bytes(int K) { return ((size_t)K * (2 * 4 + 2) + 15) / 16 * 16; }
 
 // Workgroup width (wavefronts); one workgroup per instance, looping over its
 // arms in passes of 64*w/(d/2).  The step is a chain of dependent phases per
@@ -279,6 +331,8 @@ struct StepArgs {
 // Streaming load that bypasses cache retention: every record is read once
 // per step and the state of a large batch is many times the cache size.
 typedef float nt_f4 __attribute__((ext_vector_type(4)));
+// three floats at 4-byte alignment (a record tail slice)
+typedef float nt_f3 __attribute__((ext_vector_type(3))) __attribute__((aligned(4)));
 __device__ __forceinline__ float4 ld_nt(const float4 *p) {
     const nt_f4 v = __builtin_nontemporal_load(reinterpret_cast<const nt_f4 *>(p));
     return make_float4(v.x, v.y, v.z, v.w);
@@ -391,10 +445,10 @@ struct Occupancy {
     static constexpr int waves = D == 32 ? 4 : 7;
 };
 
-template <int D>
+template <int D, int TF>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Occupancy<D>::waves)))
 void agft_step_kernel(StepArgs p) {
-    using R = Rec<D>;
+    using R = Rec<D, TF>;
     constexpr int G = R::G, S = R::S;
     constexpr int NQ = (R::R + kWave - 1) / kWave;   // update-record chunks per thread (>= 64 threads)
     const int inst = blockIdx.x;
@@ -408,7 +462,8 @@ void agft_step_kernel(StepArgs p) {
     const int j = tid % G;           // slot of this lane within its arm's group
     const int grp = tid / G;         // group index within the workgroup
     const int apw = nthr / G;        // arms per pass of the workgroup
-    const float4 *recs = p.arms + (size_t)inst * K * R::R;
+    const size_t inst_chunks = (size_t)((K + R::NB - 1) / R::NB) * R::BLK;
+    const float4 *recs = p.arms + (size_t)inst * inst_chunks;
 
     __shared__ float s_old[R::CAN];
     __shared__ float s_new[R::CAN];
@@ -504,11 +559,10 @@ void agft_step_kernel(StepArgs p) {
     // Record of the previous decision's arm: fetched now, staged in LDS before the stream.
     float4 old_chunk[NQ];
     if (upd) {
-        const float4 *src = recs + (size_t)a_upd * R::R;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
-            if (c < R::R) old_chunk[q] = ld_record<D>(src + c);
+            if (c < R::R) old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
         }
     }
 
@@ -664,11 +718,10 @@ void agft_step_kernel(StepArgs p) {
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
             if (c < R::R) {
-                const int sl = c / G, jj = c % G;
                 const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
-                    const int ci = canon(D, jj, 4 * sl + qq);
+                    const int ci = canon_chunk(D, TF, c, qq);
                     if (ci >= 0) s_old[ci] = v[qq];
                 }
             }
@@ -677,14 +730,19 @@ void agft_step_kernel(StepArgs p) {
     __syncthreads();
 
     const int nlist = s_nlist;
-    // Stream buffers: two sets of S chunks per lane, used in turn, so that one
-    // pass is scored while the next one's loads are in flight.  The first
-    // pass is issued now and lands while the update below runs.
+    // Stream buffers: two sets of S slots per lane, used in turn, so that one
+    // pass is scored while the next one's loads are in flight: the lane's
+    // main chunks, then its three tail floats.  The first pass is issued now
+    // and lands while the update below runs.
     float4 buf_a[S], buf_b[S];
     auto fetch = [&](int k, float4 *dst) {
-        const float4 *src = recs + (size_t)k * R::R + j;
+        const float4 *blk = recs + (size_t)(k / R::NB) * R::BLK;
+        const float4 *src = blk + (k % R::NB) * R::MAIN + j;
 #pragma unroll
-        for (int sidx = 0; sidx < S; ++sidx) dst[sidx] = ld_nt(src + sidx * G);
+        for (int sidx = 0; sidx < R::MQ; ++sidx) dst[sidx] = ld_nt(src + sidx * G);
+        const float *tail = reinterpret_cast<const float *>(blk + R::NB * R::MAIN + (k % R::NB) * R::TAIL) + TF * j;
+        const nt_f3 t = __builtin_nontemporal_load(reinterpret_cast<const nt_f3 *>(tail));
+        dst[R::MQ] = make_float4(t.x, t.y, t.z, 0.0f);
     };
     auto list_at = [&](int slot) { return slot < nlist ? (int)s_list[slot] : -1; };
     int k_a = -1;
@@ -739,16 +797,15 @@ void agft_step_kernel(StepArgs p) {
                 s_new[i] = fmaf(g / s_scal[0], s_scal[1], sth[i]);
             }
             __syncthreads();
-            float4 *dst = p.arms + ((size_t)inst * K + a_upd) * R::R;
+            float4 *dst = p.arms + (size_t)inst * inst_chunks;
             for (int c = tid; c < R::R; c += nthr) {
-                const int sl = c / G, jj = c % G;
                 float v[4];
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
-                    const int ci = canon(D, jj, 4 * sl + qq);
+                    const int ci = canon_chunk(D, TF, c, qq);
                     v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
                 }
-                st_record<D>(dst + c, v[0], v[1], v[2], v[3]);
+                st_record<D>(dst + rec_chunk(D, TF, a_upd, c), v[0], v[1], v[2], v[3]);
             }
             if (p.theta != nullptr && tid < D / 4) {
                 float4 *tdst = reinterpret_cast<float4 *>(p.theta + ((size_t)inst * K + a_upd) * D);
@@ -999,6 +1056,7 @@ struct InitArgs {
     StateHeader *hdr;
     StateHeader h;
     int32_t B, K, KW, d, C, IW;
+    int32_t tf;           // tail floats per lane slice
     int32_t stride0;      // stride of the starting action space
     float inv_sqrt_lambda;
 };
@@ -1006,14 +1064,17 @@ struct InitArgs {
 __global__ void agft_init_kernel(InitArgs p) {
     const size_t gtid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     const size_t gsz = (size_t)gridDim.x * blockDim.x;
-    const size_t nrec = (size_t)p.B * p.K * p.C;
-    const int G = p.d / 2;
-    for (size_t idx = gtid; idx < nrec; idx += gsz) {
-        const int c = (int)(idx % p.C);
-        const int sl = c / G, jj = c % G;
+    // every chunk of every block, the arms past K of the last block zeroed
+    const int nb = 64 / p.d, main = (p.d / 2) * (p.d / 4), tail = (p.d / 2) * p.tf / 4;
+    const int blk = nb * p.C;
+    const size_t ic = (size_t)((p.K + nb - 1) / nb) * blk;
+    for (size_t idx = gtid; idx < (size_t)p.B * ic; idx += gsz) {
+        const int o = (int)(idx % ic % blk);
+        const int k = (int)(idx % ic / blk) * nb + (o < nb * main ? o / main : (o - nb * main) / tail);
+        const int c = o < nb * main ? o % main : main + (o - nb * main) % tail;
         float v[4];
         for (int q = 0; q < 4; ++q) {
-            const int ci = canon(p.d, jj, 4 * sl + q);
+            const int ci = k < p.K ? canon_chunk(p.d, p.tf, c, q) : -1;
             v[q] = 0.0f;
             if (ci >= p.d) {
                 int i, col;
@@ -1047,18 +1108,19 @@ __global__ void agft_init_kernel(InitArgs p) {
     if (gtid == 0) *p.hdr = p.h;
 }
 
-template <int D>
+template <int D, int TF>
 __global__ void agft_export_kernel(const float4 *arms, int B, int K, float *theta, float *ainv) {
-    using R = Rec<D>;
+    using R = Rec<D, TF>;
     const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid >= (size_t)B * K) return;
     float can[R::CAN];
+    const float4 *rec = arms + (gid / K) * ((size_t)((K + R::NB - 1) / R::NB) * R::BLK);
+    const int k = (int)(gid % K);
     for (int c = 0; c < R::R; ++c) {
-        const float4 v = arms[gid * R::R + c];
+        const float4 v = rec[rec_chunk(D, TF, k, c)];
         const float vv[4] = {v.x, v.y, v.z, v.w};
-        const int sl = c / R::G, jj = c % R::G;
         for (int q = 0; q < 4; ++q) {
-            const int ci = canon(D, jj, 4 * sl + q);
+            const int ci = canon_chunk(D, TF, c, q);
             if (ci >= 0) can[ci] = vv[q];
         }
     }
@@ -1128,7 +1190,8 @@ StateHeader make_header(const agft_config *c) {
     h.B = c->B;
     h.K = c->K;
     h.d = c->d;
-    h.chunks = chunks_for(c->d);
+    h.chunks = chunks_for(c->d, tail_floats(*c));
+    h.tail_floats = tail_floats(*c);
     h.mask_words = (c->K + 31) / 32;
     h.pending = 0;
     h.t = 0;
@@ -1152,7 +1215,7 @@ extern "C" {
 
 size_t agft_state_bytes(const agft_config *cfg) {
     if (!config_ok(cfg) || !dim_supported(cfg->d)) return 0;
-    return layout_for(cfg->B, cfg->K, cfg->d, cfg->exploit).total;
+    return layout_for(*cfg).total;
 }
 
 int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stream, agft_handle **out) {
@@ -1161,7 +1224,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     if (!config_ok(cfg) || d_state == nullptr) return AGFT_E_INVAL;
     if (!dim_supported(cfg->d)) return AGFT_E_UNSUPPORTED;
     if (reinterpret_cast<uintptr_t>(d_state) % kAlign != 0) return AGFT_E_INVAL;
-    const Layout lay = layout_for(cfg->B, cfg->K, cfg->d, cfg->exploit);
+    const Layout lay = layout_for(*cfg);
     if (nbytes < lay.total) return AGFT_E_INVAL;
     agft_handle *h = new (std::nothrow) agft_handle;
     if (h == nullptr) return AGFT_E_INVAL;
@@ -1181,7 +1244,8 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
             return AGFT_E_HIP;
         }
         if (got.magic != kMagic || got.version != want.version || got.B != want.B || got.K != want.K ||
-            got.d != want.d || got.chunks != want.chunks || got.exploit != want.exploit || got.t < 0 ||
+            got.d != want.d || got.chunks != want.chunks || got.tail_floats != want.tail_floats ||
+            got.exploit != want.exploit || got.t < 0 ||
             (got.pending != 0 && got.pending != 1)) {
             delete h;
             return AGFT_E_STATE;
@@ -1203,7 +1267,8 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     a.K = cfg->K;
     a.KW = (cfg->K + 31) / 32;
     a.d = cfg->d;
-    a.C = chunks_for(cfg->d);
+    a.tf = tail_floats(*cfg);
+    a.C = chunks_for(cfg->d, a.tf);
     a.IW = inst_words(cfg->d);
     a.stride0 = cfg->refine ? cfg->refine_stride : 1;
     a.inv_sqrt_lambda = (float)(1.0 / std::sqrt((double)cfg->lambda));
@@ -1268,10 +1333,20 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.early_update = explore_bytes(c) <= 16384 ? 1 : 0;
     const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves));
     const size_t lds = step_lds_bytes(c.K);
+    const bool packed_tails = tail_floats(c) == 3;
     switch (c.d) {
-        case 8: hipLaunchKernelGGL(agft_step_kernel<8>, grid, block, lds, h->stream, p); break;
-        case 16: hipLaunchKernelGGL(agft_step_kernel<16>, grid, block, lds, h->stream, p); break;
-        case 32: hipLaunchKernelGGL(agft_step_kernel<32>, grid, block, lds, h->stream, p); break;
+        case 8:
+            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<8, 3>), grid, block, lds, h->stream, p);
+            else hipLaunchKernelGGL((agft_step_kernel<8, 4>), grid, block, lds, h->stream, p);
+            break;
+        case 16:
+            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<16, 3>), grid, block, lds, h->stream, p);
+            else hipLaunchKernelGGL((agft_step_kernel<16, 4>), grid, block, lds, h->stream, p);
+            break;
+        case 32:
+            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<32, 3>), grid, block, lds, h->stream, p);
+            else hipLaunchKernelGGL((agft_step_kernel<32, 4>), grid, block, lds, h->stream, p);
+            break;
         default: return AGFT_E_UNSUPPORTED;
     }
     const hipError_t e = hipGetLastError();
@@ -1292,7 +1367,9 @@ int agft_get_state(const agft_handle *h, agft_state_view *out) {
     out->B = h->cfg.B;
     out->K = h->cfg.K;
     out->d = h->cfg.d;
-    out->chunks = chunks_for(h->cfg.d);
+    out->tail_floats = tail_floats(h->cfg);
+    out->chunks = chunks_for(h->cfg.d, out->tail_floats);
+    out->block_arms = block_arms(h->cfg.d);
     out->mask_words = (h->cfg.K + 31) / 32;
     out->arms = h->base + h->lay.arms;
     out->mask = at<uint32_t>(h->base, h->lay.mask);
@@ -1310,10 +1387,20 @@ int agft_export(agft_handle *h, float *d_theta, float *d_ainv) {
     const size_t n = (size_t)c.B * c.K;
     const dim3 grid((unsigned)((n + 127) / 128)), block(128);
     const float4 *arms = at<float4>(h->base, h->lay.arms);
+    const bool packed_tails = tail_floats(c) == 3;
     switch (c.d) {
-        case 8: hipLaunchKernelGGL(agft_export_kernel<8>, grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv); break;
-        case 16: hipLaunchKernelGGL(agft_export_kernel<16>, grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv); break;
-        case 32: hipLaunchKernelGGL(agft_export_kernel<32>, grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv); break;
+        case 8:
+            if (packed_tails) hipLaunchKernelGGL((agft_export_kernel<8, 3>), grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv);
+            else hipLaunchKernelGGL((agft_export_kernel<8, 4>), grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv);
+            break;
+        case 16:
+            if (packed_tails) hipLaunchKernelGGL((agft_export_kernel<16, 3>), grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv);
+            else hipLaunchKernelGGL((agft_export_kernel<16, 4>), grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv);
+            break;
+        case 32:
+            if (packed_tails) hipLaunchKernelGGL((agft_export_kernel<32, 3>), grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv);
+            else hipLaunchKernelGGL((agft_export_kernel<32, 4>), grid, block, 0, h->stream, arms, c.B, c.K, d_theta, d_ainv);
+            break;
         default: return AGFT_E_UNSUPPORTED;
     }
     return hip_status(hipGetLastError());

@@ -119,10 +119,13 @@ class Tuner:
             return self.state[off:off + nb].view(dtype).view(shape)
 
         B, K, d, C, KW, IW = v.B, v.K, v.d, v.chunks, v.mask_words, v.inst_words
+        NB = v.block_arms
+        KB = (K + NB - 1) // NB
         inst = region(v.inst, B * IW, torch.int32, (B, IW))
         return dict(
             t=int(v.t), pending=int(v.pending),
-            arms=region(v.arms, B * K * C * 4, torch.float32, (B, K, C, 4)),
+            # [B][blocks][NB * chunks][4]: per block the NB main parts, then the NB tails
+            arms=region(v.arms, B * KB * NB * C * 4, torch.float32, (B, KB, NB * C, 4)),
             mask=region(v.mask, B * KW, torch.int32, (B, KW)),
             inst=inst,
             aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2], mode=inst[:, 3], ph=inst[:, 3:12],

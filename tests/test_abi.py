@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert L.agft_abi_version() == L.ABI_VERSION == 3
+    assert L.agft_abi_version() == L.ABI_VERSION == 4
     for code in (0, -1, -2, -3, -4):
         assert L.agft_strerror(code)
     assert L.agft_strerror(-99) == "unknown status"
@@ -53,12 +53,27 @@ def test_state_bytes(lib):
     good = dict(prune_rule=15, ext_rounds=60, ext_min_n=3, ext_thr=-1.2, hist_after=30, hist_min_n=6,
                 hist_kappa=1.0, hist_min_arms=3, cascade_k=16)
     assert L.agft_state_bytes(_cfg(**good)) == n
-    # the arm records dominate: B * K * (d/2) * ((d+6)/4) float4 chunks
-    # (d + d(d+1)/2 floats per arm, padded to whole chunks per lane slice)
-    for d, chunks in ((8, 12), (16, 40), (32, 144)):
-        assert 4 * chunks >= d + d * (d + 1) // 2
+    # the arm records dominate: B * K * (d/2) * (d+3)/4 float4 chunks, exactly
+    # the d + d(d+1)/2 floats of theta and S per arm, with no padding
+    for d, chunks in ((8, 11), (16, 38), (32, 140)):
+        assert 4 * chunks == d + d * (d + 1) // 2
         big = L.agft_state_bytes(_cfg(B=4096, K=128, d=d))
-        assert 4096 * 128 * chunks * 16 <= big < 4096 * 128 * chunks * 16 * 1.05
+        # beyond the records: stats (8 B per arm), instance blocks (<= 256 B),
+        # mask words, header and alignment
+        assert 0 <= big - 4096 * 128 * chunks * 16 < 4096 * (128 * 8 + 256 + 16) + 1024
+    # K is rounded up to whole blocks of 64/d arms: K=125 at d=16 takes 128 slots
+    # (the other regions of K=125 add less than the 3 slots' 7.5 MB)
+    assert L.agft_state_bytes(_cfg(B=4096, K=125, d=16)) >= 4096 * 128 * 38 * 16
+    # up to 16 KB of records per exploring instance (26 arms of 608 bytes at
+    # d=16) the tails are padded to whole chunks: 40 chunks per record, so
+    # K=26 (28 slots of 640 bytes) needs more than K=27 (28 slots of 608)
+    b26, b27 = (L.agft_state_bytes(_cfg(B=4096, K=k, d=16)) for k in (26, 27))
+    assert 4096 * 28 * 40 * 16 <= b26 and b27 < b26 and b27 - 4096 * 28 * 38 * 16 < 4096 * (27 * 8 + 272) + 1024
+    # the refinement counts the arms in play: K=128 with windows of 21 arms
+    # and a coarse grid of 13 streams 12.8 KB, padded tails
+    ref = dict(refine=1, refine_period=50, refine_stride=10, refine_half=10, refine_mature=100,
+               refine_min_n=4)
+    assert L.agft_state_bytes(_cfg(B=4096, K=128, d=16, **ref)) >= 4096 * 128 * 40 * 16
     for bad in (dict(B=0), dict(K=0), dict(K=1025), dict(lambda_=0.0), dict(lambda_=float("nan")),
                 dict(alpha0=-1.0), dict(alpha0=float("inf")), dict(alpha_sched=2),
                 dict(prune_rule=16), dict(prune_rule=-1), dict(prune_period=0), dict(flags=4), dict(d=12),
