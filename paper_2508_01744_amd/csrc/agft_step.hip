@@ -488,6 +488,7 @@ void agft_step_kernel(StepArgs p) {
     __shared__ int s_red_k2[kMaxWaves];
 
     __shared__ float s_xp[D];   // context of the previous decision, for the update
+    __shared__ int2 s_stu;      // its arm's reward count and sum
 
     const bool decide = p.ctx != nullptr;
 
@@ -557,13 +558,18 @@ void agft_step_kernel(StepArgs p) {
                                : __float_as_int(pick<6>(ph, tid - kInstPh));
 
     // Record of the previous decision's arm: fetched now, staged in LDS before the stream.
+    // Its reward count and sum are fetched now as well: read at update time
+    // they would wait behind the record's write-back (stores and loads share
+    // one completion counter), about 6 us per workgroup.
     float4 old_chunk[NQ];
+    int2 st_upd = make_int2(0, 0);
     if (upd) {
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
             if (c < R::R) old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
         }
+        if (tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
     }
 
     // the arms in play: not removed by a pruning rule, inside the action space
@@ -714,6 +720,7 @@ void agft_step_kernel(StepArgs p) {
     // The previous decision's record, fetched at kernel start, goes to LDS in
     // canonical order now, so that it holds no registers through the stream.
     if (upd) {
+        if (tid == 0) s_stu = st_upd;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
@@ -811,11 +818,9 @@ void agft_step_kernel(StepArgs p) {
                 float4 *tdst = reinterpret_cast<float4 *>(p.theta + ((size_t)inst * K + a_upd) * D);
                 tdst[tid] = make_float4(s_new[4 * tid], s_new[4 * tid + 1], s_new[4 * tid + 2], s_new[4 * tid + 3]);
             }
-            if (tid == 0) {
-                int2 &sa = p.stats[(size_t)inst * K + a_upd];
-                const int2 v = sa;
-                sa = make_int2(v.x + 1, __float_as_int(__int_as_float(v.y) + r));
-            }
+            if (tid == 0)
+                p.stats[(size_t)inst * K + a_upd] =
+                    make_int2(s_stu.x + 1, __float_as_int(__int_as_float(s_stu.y) + r));
         } else if (has_prev && tid == 0) {
             blk[kInstBad] += 1;
         }
