@@ -7,6 +7,7 @@ Open loop (the same contexts and rewards to both sides); afterwards the
 final models are compared through the export kernel, and the raw records
 are checked for what the layout promises: zero padding floats with padded
 tails, and zero slots past K in the last block."""
+import numpy as np
 import pytest
 import torch
 
@@ -15,6 +16,31 @@ from gpu_helpers import compare_model, random_contexts, run_open_loop, say
 from paper_2508_01744_amd import _lib as L
 
 pytestmark = pytest.mark.gpu
+
+
+def _decode(arms, K, d, tf):
+    """theta [B][K][d] and the upper-triangular factor S [B][K][d][d] from the
+    raw records [B][blocks][NB*chunks][4], following the layout that
+    include/agft.h documents for agft_state_view.arms."""
+    B = arms.shape[0]
+    G, nb = d // 2, 64 // d
+    M, T = G * (d // 4), G * tf // 4
+    theta = np.zeros((B, K, d), np.float32)
+    S = np.zeros((B, K, d, d), np.float32)
+    for k in range(K):
+        blk, r = arms[:, k // nb], k % nb
+        main = blk[:, r * M:(r + 1) * M]                          # [B][M][4]
+        tail = blk[:, nb * M + r * T:nb * M + (r + 1) * T].reshape(B, -1)
+        for j in range(G):
+            for e in range(d + 3):
+                v = main[:, (e // 4) * G + j, e % 4] if e < d else tail[:, tf * j + e - d]
+                if e <= j:
+                    S[:, k, e, j] = v
+                elif e <= d:
+                    S[:, k, d - e, d - 1 - j] = v
+                else:
+                    theta[:, k, 2 * j + e - d - 1] = v
+    return theta, S
 
 # (d, K, expected tail floats): K*4*(d + d(d+1)/2) bytes against 16 KB, and
 # K % (64/d) != 0 in every case
@@ -47,6 +73,13 @@ def test_layout_open_loop(d, K, tf):
     if tf == 4:                                        # float 4j+3 of every tail slice
         tails = arms[:, :, nb * MAIN:, :]
         assert not tails[..., 3].any()
+    # the records decoded as the header documents them give the exported model
+    theta, S = _decode(arms, K, d, tf)
+    th, ai = tuner.export(theta=True, ainv=True)
+    assert np.array_equal(theta, th.cpu().numpy())
+    ainv = np.einsum("bkij,bklj->bkil", S.astype(np.float64), S.astype(np.float64))
+    ref = ai.cpu().numpy().astype(np.float64)
+    assert np.abs(ainv - ref).max() <= 1e-5 * max(1.0, np.abs(ref).max())
     say(f"[layout] d={d} K={K}: max score err {st['max_score_err']:.2e}, "
         f"forced {st['forced']}/{st['decisions']}")
     torch.cuda.synchronize()
