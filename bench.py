@@ -63,13 +63,16 @@ def step_bytes(wl, scored_exploring, scored_greedy, mask_write, update):
     return float(records + io + mask)
 
 
-def cpu_baseline(wl, budget_s):
+def cpu_baseline(wl, budget_s, threads=None, n_max=16384):
     """The fp64 oracle (C, OpenMP over instances) with its fp64 environment,
-    closed loop, on a bounded sample of the workload's instances and steps."""
-    import numpy as np
+    closed loop, on a bounded sample of the workload's instances and steps
+    (threads: the OpenMP thread count, default all)."""
     from agft_workloads import exogenous
     from oracle import Env, Oracle
-    n = min(wl.B, 16384)
+    n = min(wl.B, n_max)
+    all_threads = Oracle.threads()
+    if threads is not None:
+        Oracle.set_threads(threads)
     T = wl.T
     arr, noi = exogenous(wl, range(n), T)
     env = Env(wl, arr, noi, T)
@@ -86,7 +89,9 @@ def cpu_baseline(wl, budget_s):
         if time.perf_counter() - t0 > budget_s:
             break
     el = time.perf_counter() - t0
-    return dict(value=n * steps / el, unit="decision-steps/s", cores=Oracle.threads(), kind="oracle",
+    cores = Oracle.threads()
+    Oracle.set_threads(all_threads)
+    return dict(value=n * steps / el, unit="decision-steps/s", cores=cores, kind="oracle",
                 sample=f"{n} instances x {steps} steps of {wl.name} (closed loop with the fp64 "
                        f"environment, {el:.1f} s)")
 
@@ -250,6 +255,8 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
+        one = cpu_baseline(wl, args.cpu_budget / 3, threads=1, n_max=1024)
+        res["detail"]["cpu_oracle_1thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
     print(json.dumps(res), flush=True)
 
 
