@@ -63,7 +63,7 @@ def step_bytes(wl, scored_exploring, scored_greedy, mask_write, update):
     return float(records + io + mask)
 
 
-def cpu_baseline(wl, budget_s, threads=None, n_max=16384):
+def cpu_baseline(wl, budget_s, threads=None, n_max=16384, max_steps=None):
     """The fp64 oracle (C, OpenMP over instances) with its fp64 environment,
     closed loop, on a bounded sample of the workload's instances and steps
     (threads: the OpenMP thread count, default all)."""
@@ -81,7 +81,7 @@ def cpu_baseline(wl, budget_s, threads=None, n_max=16384):
     r = None
     t0 = time.perf_counter()
     steps = 0
-    for t in range(T):
+    for t in range(T if max_steps is None else min(T, max_steps)):
         ucb, lcb, keep, action = ora.decide(x, r)
         ora.commit(x, action, keep)
         r, x = env.step(t, action)
@@ -93,7 +93,7 @@ def cpu_baseline(wl, budget_s, threads=None, n_max=16384):
     Oracle.set_threads(all_threads)
     return dict(value=n * steps / el, unit="decision-steps/s", cores=cores, kind="oracle",
                 sample=f"{n} instances x {steps} steps of {wl.name} (closed loop with the fp64 "
-                       f"environment, {el:.1f} s)")
+                       f"environment, {el:.1f} s)", n=n, steps=steps)
 
 
 def main():
@@ -254,8 +254,12 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
-        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_budget)
-        one = cpu_baseline(wl, args.cpu_budget / 3, threads=1, n_max=1024)
+        base = cpu_baseline(wl, args.cpu_budget)
+        # one thread over the same steps (the step mix changes as arms are
+        # pruned) on a third of one thread's share of the instances
+        one = cpu_baseline(wl, args.cpu_budget, threads=1, max_steps=base["steps"],
+                           n_max=max(1, base["n"] // (3 * base["cores"])))
+        res["cpu_baseline"] = {k: base[k] for k in ("value", "unit", "cores", "kind", "sample")}
         res["detail"]["cpu_oracle_1thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
     print(json.dumps(res), flush=True)
 
