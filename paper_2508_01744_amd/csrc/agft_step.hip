@@ -223,13 +223,19 @@ size_t step_lds_bytes(int K) { return ((size_t)K * (2 * 4 + 2) + 15) / 16 * 16; 
 //   the same, refinement (13 KB):          190 / 231 / 376
 //   K=256 d=32 B=1,024 (590 KB):           31 / 29 / 29
 //   the same, exploitation (32 KB):        43 / 34 / 31
-// Where an exploring instance streams at most 16 KB, the update of the
-// previous decision's arm also runs before the stream rather than after it
-// (K=64 d=8: 20.5 -> 19.1 us; K=128 d=16 B=65,536 would lose 3%).
 int waves_for(const agft_config &c) {
     const size_t bytes = c.exploit ? (size_t)arms_in_play(c) * 4 * c.d : explore_bytes(c);
     return bytes <= 16384 ? 1 : 4;
 }
+
+// Whether the update of the previous decision's arm runs before the stream
+// (its first pass lands meanwhile and the chain gets shorter) rather than
+// after it: always, except at d = 32 where an instance streams more than
+// 16 KB, since there the longer update holds back the second pass.
+// Measured on MI355X (step kernel, before / after the stream): K=64 d=8
+// B=4,096 19.1 / 20.5 us; K=128 d=16 B=65,536 853 / 857 us, B=16,384 218.4 /
+// 220.8 us; K=256 d=32 B=1,024 92.4 / 91.7 us.
+bool early_update(const agft_config &c) { return c.d < 32 || explore_bytes(c) <= 16384; }
 
 // Per-lane slice of the Eq. 1 terms from the S chunks of one record slice:
 // va, vb = the two owned entries of S^T x, m = the two owned theta terms.
@@ -1335,7 +1341,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
     const int waves = waves_for(c);
-    p.early_update = explore_bytes(c) <= 16384 ? 1 : 0;
+    p.early_update = early_update(c) ? 1 : 0;
     const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves));
     const size_t lds = step_lds_bytes(c.K);
     const bool packed_tails = tail_floats(c) == 3;
