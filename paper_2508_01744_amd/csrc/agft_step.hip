@@ -699,20 +699,19 @@ void agft_step_kernel(StepArgs p) {
         __syncthreads();
     }
 
-    // Active arms other than the one being updated, in index order.
+    // Active arms other than the one being updated, in index order: one arm
+    // per lane, 64 at a time, each placed by the count of active lanes below
+    // it in the wavefront's ballot.
     if (wave == 0) {
-        uint32_t wl = lane < KW ? s_mask[lane] : 0u;
-        if (x_ok && a_upd >= 0 && (a_upd >> 5) == lane) wl &= ~(1u << (a_upd & 31));
-        if (!x_ok) wl = 0u;
-        const int cnt = __popc(wl);
-        const int incl = scan32(cnt);
-        int pos = incl - cnt;
-        while (wl) {
-            const int b = __ffs(wl) - 1;
-            s_list[pos++] = (short)(32 * lane + b);
-            wl &= wl - 1;
+        int placed = 0;
+        for (int k0 = 0; k0 < K; k0 += kWave) {
+            const int k = k0 + lane;
+            const bool on = x_ok && k < K && k != a_upd && ((s_mask[k >> 5] >> (k & 31)) & 1u) != 0u;
+            const unsigned long long bal = __ballot(on);
+            if (on) s_list[placed + __popcll(bal & ((1ull << lane) - 1ull))] = (short)k;
+            placed += __popcll(bal);
         }
-        if (lane == kMaxWords - 1) s_nlist = incl;
+        if (lane == 0) s_nlist = placed;
     }
 
     // This lane's selectors of x: xa_e = x_e for e <= j, xb_e = x_{D-e} for e > j.
