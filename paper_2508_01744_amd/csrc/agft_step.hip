@@ -140,6 +140,33 @@ __host__ __device__ constexpr int canon_chunk(int D, int TF, int c, int q) {
     return t % TF < 3 ? canon(D, t / TF, D + t % TF) : -1;
 }
 
+// Canonical indices of the four components of every record chunk (-1 for
+// padding), built at compile time and read from constant memory, one 8-byte
+// load per chunk, instead of being recomputed by each thread.
+template <int D, int TF>
+struct ChunkMap {
+    int16_t ci[(D / 2) * (D / 4) + (D / 2) * TF / 4][4];
+};
+template <int D, int TF>
+constexpr ChunkMap<D, TF> make_chunk_map() {
+    ChunkMap<D, TF> m{};
+    for (int c = 0; c < (D / 2) * (D / 4) + (D / 2) * TF / 4; ++c)
+        for (int q = 0; q < 4; ++q) m.ci[c][q] = (int16_t)canon_chunk(D, TF, c, q);
+    return m;
+}
+template <int D, int TF>
+__constant__ ChunkMap<D, TF> kChunkMap = make_chunk_map<D, TF>();
+
+template <int D, int TF>
+__device__ __forceinline__ int2 ld_chunk_map(int c) {
+    return *reinterpret_cast<const int2 *>(&kChunkMap<D, TF>.ci[c][0]);
+}
+// component q of a chunk's map entry
+__device__ __forceinline__ int map_at(int2 m, int q) {
+    const int w = q < 2 ? m.x : m.y;
+    return (q & 1) ? (w >> 16) : (int)(int16_t)(w & 0xffff);
+}
+
 // Column j and row i of packed element e.
 __device__ inline void unpack(int e, int &i, int &j) {
     int c = 0;
@@ -568,12 +595,17 @@ void agft_step_kernel(StepArgs p) {
     // they would wait behind the record's write-back (stores and loads share
     // one completion counter), about 6 us per workgroup.
     float4 old_chunk[NQ];
+    int2 cmap[NQ];   // canonical indices of those chunks
     int2 st_upd = make_int2(0, 0);
     if (upd) {
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
-            if (c < R::R) old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
+            cmap[q] = make_int2(0, 0);
+            if (c < R::R) {
+                old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
+                cmap[q] = ld_chunk_map<D, TF>(c);
+            }
         }
         if (tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
     }
@@ -733,7 +765,7 @@ void agft_step_kernel(StepArgs p) {
                 const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
-                    const int ci = canon_chunk(D, TF, c, qq);
+                    const int ci = map_at(cmap[q], qq);
                     if (ci >= 0) s_old[ci] = v[qq];
                 }
             }
@@ -767,7 +799,7 @@ void agft_step_kernel(StepArgs p) {
     // Run before the stream when each instance streams little (its first
     // pass lands meanwhile and the chain gets shorter), after it otherwise
     // (the update would hold back the stream's second pass).
-    auto update = [&]() {
+    auto update = [&](const int2 *cm) {
         if (upd) {
             const float *sth = s_old;         // theta
             const float *sS = s_old + D;      // packed factor
@@ -810,14 +842,18 @@ void agft_step_kernel(StepArgs p) {
             }
             __syncthreads();
             float4 *dst = p.arms + (size_t)inst * inst_chunks;
-            for (int c = tid; c < R::R; c += nthr) {
-                float v[4];
 #pragma unroll
-                for (int qq = 0; qq < 4; ++qq) {
-                    const int ci = canon_chunk(D, TF, c, qq);
-                    v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
+            for (int q = 0; q < NQ; ++q) {
+                const int c = tid + q * nthr;
+                if (c < R::R) {
+                    float v[4];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) {
+                        const int ci = map_at(cm[q], qq);
+                        v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
+                    }
+                    st_record<D>(dst + rec_chunk(D, TF, a_upd, c), v[0], v[1], v[2], v[3]);
                 }
-                st_record<D>(dst + rec_chunk(D, TF, a_upd, c), v[0], v[1], v[2], v[3]);
             }
             if (p.theta != nullptr && tid < D / 4) {
                 float4 *tdst = reinterpret_cast<float4 *>(p.theta + ((size_t)inst * K + a_upd) * D);
@@ -831,7 +867,7 @@ void agft_step_kernel(StepArgs p) {
         }
     };
     const bool early = p.early_update && !greedy;   // an exploiting instance has no pass in flight
-    if (early) update();
+    if (early) update(cmap);
 
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
     if (greedy) {
@@ -891,7 +927,17 @@ void agft_step_kernel(StepArgs p) {
         }
     }
 
-    if (!early) update();
+    if (!early) {
+        // the chunk map again (registers held through the stream would cost
+        // occupancy); its load overlaps the update's first phase
+        int2 cml[NQ];
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+            const int c = tid + q * nthr;
+            cml[q] = upd && c < R::R ? ld_chunk_map<D, TF>(c) : make_int2(0, 0);
+        }
+        update(cml);
+    }
 
     // the updated arm, scored on x_t from LDS in the streaming order
     if (upd && x_ok && wave == 0) {
