@@ -36,8 +36,10 @@ def test_single_arm(d):
     assert (a == 0).all()
 
 
-def test_max_arms():
-    _open_loop_case("K=1024 d=8", _cfg(3, 1024, 8, prune=1, period=20), 60, 2)
+@pytest.mark.parametrize("d,T", [(8, 60), (16, 50), (32, 40)])
+def test_max_arms(d, T):
+    """K = 1024, the largest arm count: 2.3 MB of records per instance at d = 32."""
+    _open_loop_case(f"K=1024 d={d}", _cfg(3, 1024, d, prune=1, period=20), T, 2)
 
 
 @pytest.mark.parametrize("K", [63, 65, 100, 129, 255])
