@@ -243,7 +243,9 @@ size_t step_lds_bytes(int K) { return ((size_t)K * (2 * 4 + 2) + 15) / 16 * 16; 
 // step are estimated from the arms in play (with the refinement, at most the
 // larger of the coarse grid and the window) times what each costs (the
 // record, or the theta copy once instances exploit): one wavefront up to
-// 16 KB, four beyond.  Measured on MI355X (step kernel, us, w = 1 / 2 / 4):
+// 16 KB, four beyond.  Measured on MI355X with padded 640-byte records
+// (step kernel, us, w = 1 / 2 / 4; with the packed blocks, w = 2 stayed
+// 2-3% slower than w = 4 at K=128 d=16):
 //   K=64 d=8 B=4,096 (12 KB):              21 / 25 / 30
 //   K=128 d=16 B=65,536 (80 KB):           895 / 892 / 882
 //   the same, exploitation (8 KB):         595 / 602 / 672
@@ -796,9 +798,8 @@ void agft_step_kernel(StepArgs p) {
     }
 
     // ---- square-root rank-1 update of the previous decision's arm ----
-    // Run before the stream when each instance streams little (its first
-    // pass lands meanwhile and the chain gets shorter), after it otherwise
-    // (the update would hold back the stream's second pass).
+    // Run while the stream's first pass is in flight, or after the stream
+    // (early_update on the host decides which).
     auto update = [&](const int2 *cm) {
         if (upd) {
             const float *sth = s_old;         // theta
