@@ -32,6 +32,18 @@ def source_hash(path=STEP_SRC):
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
+def counter_traffic(workload, path=COUNTERS, source=STEP_SRC):
+    """HBM bytes per step-kernel launch from the committed counter summary,
+    or None unless it was taken on this workload with this kernel source."""
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        cnt = json.load(fh)
+    if cnt.get("source_sha256_16") != source_hash(source) or cnt.get("workload") != workload:
+        return None
+    return cnt.get("hbm_bytes_per_launch")
+
+
 def record_floats(d):
     return d + d * (d + 1) // 2
 
@@ -218,12 +230,7 @@ def main():
     kernel_avg_ms = float(kernel_ms.mean())
     achieved = bytes_per_launch / (kernel_avg_ms * 1e-3) / 1e9
 
-    traffic = None
-    if os.path.exists(COUNTERS):
-        with open(COUNTERS) as fh:
-            cnt = json.load(fh)
-        if cnt.get("source_sha256_16") == source_hash() and cnt.get("workload") == wl.name:
-            traffic = cnt.get("hbm_bytes_per_launch")
+    traffic = counter_traffic(wl.name)
 
     value = wl.B * K / (elapsed_ms * 1e-3)
     res = {
