@@ -32,6 +32,55 @@ def source_hash(path=STEP_SRC):
         return hashlib.sha256(fh.read()).hexdigest()[:16]
 
 
+class TimingEvent:
+    """A HIP event for timing only, recorded on a torch stream: created with
+    hipEventDisableSystemFence, so that recording it does not write back and
+    invalidate the caches the way a default event does (that costs about
+    3 us per record and lands on the launch being timed)."""
+    _hip = None
+    FLAGS = 0x20000000   # hipEventDisableSystemFence
+
+    @classmethod
+    def _lib(cls):
+        if cls._hip is None:
+            import ctypes
+            lib = ctypes.CDLL("libamdhip64.so")
+            vp = ctypes.c_void_p
+            lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+            lib.hipEventRecord.argtypes = [vp, vp]
+            lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+            lib.hipEventDestroy.argtypes = [vp]
+            for f in (lib.hipEventCreateWithFlags, lib.hipEventRecord, lib.hipEventElapsedTime,
+                      lib.hipEventDestroy):
+                f.restype = ctypes.c_int
+            cls._hip = lib
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        self._ev = ctypes.c_void_p()
+        rc = self._lib().hipEventCreateWithFlags(ctypes.byref(self._ev), self.FLAGS)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def record(self, stream):
+        rc = self._lib().hipEventRecord(self._ev, stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
+
+    def elapsed_time(self, end):
+        import ctypes
+        ms = ctypes.c_float()
+        rc = self._lib().hipEventElapsedTime(ctypes.byref(ms), self._ev, end._ev)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and getattr(self, "_ev", None):
+            self._hip.hipEventDestroy(self._ev)
+
+
 def counter_traffic(workload, path=COUNTERS, source=STEP_SRC):
     """HBM bytes per step-kernel launch from the committed counter summary,
     or None unless it was taken on this workload with this kernel source."""
@@ -187,7 +236,7 @@ def main():
     fresh()
     torch.cuda.synchronize()
 
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    ev = [(TimingEvent(), TimingEvent()) for _ in range(K)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
