@@ -44,7 +44,10 @@ class TimingEvent:
     def _lib(cls):
         if cls._hip is None:
             import ctypes
-            lib = ctypes.CDLL("libamdhip64.so")
+            from paper_2508_01744_amd import _lib
+            # the HIP runtime the step kernel's library is bound to (symbol
+            # lookup through its handle reaches its dependencies)
+            lib = ctypes.CDLL(_lib.LIB_PATH)
             vp = ctypes.c_void_p
             lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
             lib.hipEventRecord.argtypes = [vp, vp]
