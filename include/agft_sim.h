@@ -62,7 +62,7 @@ size_t agft_env_state_bytes(const agft_env_config *cfg);
  * d_env       [agft_env_state_bytes] device buffer, 256-byte aligned, caller-owned.
  * d_arrivals  int32 [T+1][B] arrivals per window (time-major), device.
  * d_noise     fp32 [T+1][B] latency noise per window, device.
- * d_ctx       fp32 [B][d] out: x_0.
+ * d_ctx       fp32 [B][d] out: x_0, 16-byte aligned.
  * stream      hipStream_t (NULL = null stream).
  */
 int agft_env_reset(const agft_env_config *cfg, void *d_env, size_t nbytes, const int32_t *d_arrivals,
@@ -72,7 +72,7 @@ int agft_env_reset(const agft_env_config *cfg, void *d_env, size_t nbytes, const
  * Run window t+1 at the clock of decision t (0 <= t < T) for every instance.
  * d_action    int32 [B]: a_t (-1 keeps the previous clock).
  * d_reward    fp32 [B] out: reward of decision t.
- * d_ctx       fp32 [B][d] out: x_{t+1}.
+ * d_ctx       fp32 [B][d] out: x_{t+1}, 16-byte aligned.
  */
 int agft_env_step(const agft_env_config *cfg, void *d_env, size_t nbytes, int32_t t,
                   const int32_t *d_action, const int32_t *d_arrivals, const float *d_noise,

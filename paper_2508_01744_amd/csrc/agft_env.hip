@@ -69,9 +69,11 @@ __device__ inline int arm_capacity(const EnvArgs &p, int k) {
     return (int)((2 * num + den) / (2 * den));
 }
 
-__global__ void agft_env_kernel(EnvArgs p) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= p.B) return;
+constexpr int kEnvThreads = 256;
+
+// One instance's window: state update, reward and the next context, which
+// goes to xs (d/4 float4 slots).
+__device__ __forceinline__ void env_instance(const EnvArgs &p, int i, float4 *xs) {
     const size_t B = (size_t)p.B;
     int q, cap;
     float f;
@@ -141,7 +143,9 @@ __global__ void agft_env_kernel(EnvArgs p) {
     p.cap[i] = cap;
     p.f[i] = f;
 
-    float *x = p.ctx + (size_t)i * p.d;
+    float x[32];
+#pragma unroll
+    for (int k = 0; k < 32; ++k) x[k] = 0.0f;
     x[0] = 1.0f;
 #pragma unroll
     for (int j = 0; j < kZ; ++j) x[1 + j] = zl[0][j];
@@ -157,6 +161,23 @@ __global__ void agft_env_kernel(EnvArgs p) {
 #pragma unroll
         for (int l = 0; l < kRLags; ++l) x[29 + l] = rl[l];
     }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+        if (4 * q < p.d) xs[q] = make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
+}
+
+// One thread per instance.  Each context goes through LDS so that the
+// block's contexts (contiguous in the output) leave as whole-line float4
+// stores rather than d strided words per thread.
+__global__ __launch_bounds__(kEnvThreads) void agft_env_kernel(EnvArgs p) {
+    __shared__ float4 s_ctx[kEnvThreads * 32 / 4];
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < p.B) env_instance(p, i, s_ctx + threadIdx.x * (p.d / 4));
+    __syncthreads();
+    const int i0 = blockIdx.x * blockDim.x;
+    const int n = p.B - i0 < (int)blockDim.x ? p.B - i0 : (int)blockDim.x;
+    float4 *dst = reinterpret_cast<float4 *>(p.ctx + (size_t)i0 * p.d);
+    for (int c = threadIdx.x; c < n * p.d / 4; c += blockDim.x) dst[c] = s_ctx[c];
 }
 
 bool env_config_ok(const agft_env_config *c) {
@@ -211,8 +232,8 @@ EnvArgs make_args(const agft_env_config *c, void *d_env) {
 }
 
 int launch(const EnvArgs &p, void *stream) {
-    const unsigned blocks = (unsigned)((p.B + 255) / 256);
-    hipLaunchKernelGGL(agft_env_kernel, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), p);
+    const unsigned blocks = (unsigned)((p.B + kEnvThreads - 1) / kEnvThreads);
+    hipLaunchKernelGGL(agft_env_kernel, dim3(blocks), dim3(kEnvThreads), 0, static_cast<hipStream_t>(stream), p);
     return hipGetLastError() == hipSuccess ? AGFT_OK : AGFT_E_HIP;
 }
 
@@ -230,6 +251,7 @@ int agft_env_reset(const agft_env_config *cfg, void *d_env, size_t nbytes, const
     if (!env_config_ok(cfg)) return AGFT_E_INVAL;
     if (d_env == nullptr || d_arrivals == nullptr || d_noise == nullptr || d_ctx == nullptr)
         return AGFT_E_INVAL;
+    if (reinterpret_cast<uintptr_t>(d_ctx) % 16 != 0) return AGFT_E_INVAL;
     if (reinterpret_cast<uintptr_t>(d_env) % kAlign != 0 || nbytes < env_layout(cfg->B).total)
         return AGFT_E_INVAL;
     EnvArgs p = make_args(cfg, d_env);
@@ -251,6 +273,7 @@ int agft_env_step(const agft_env_config *cfg, void *d_env, size_t nbytes, int32_
     if (d_env == nullptr || d_action == nullptr || d_arrivals == nullptr || d_noise == nullptr ||
         d_reward == nullptr || d_ctx == nullptr)
         return AGFT_E_INVAL;
+    if (reinterpret_cast<uintptr_t>(d_ctx) % 16 != 0) return AGFT_E_INVAL;
     if (reinterpret_cast<uintptr_t>(d_env) % kAlign != 0 || nbytes < env_layout(cfg->B).total)
         return AGFT_E_INVAL;
     if (t < 0 || t >= cfg->T) return AGFT_E_INVAL;

@@ -148,6 +148,10 @@ def test_env_validation(lib):
     assert L.agft_env_step(cfg, p, n, -1, p, p, p, p, p, None) == L.AGFT_E_INVAL
     assert L.agft_env_step(cfg, p, n, cfg.T, p, p, p, p, p, None) == L.AGFT_E_INVAL
     assert L.agft_env_step(cfg, p, n, 0, None, p, p, p, p, None) == L.AGFT_E_INVAL
+    # contexts leave as float4 stores: a context buffer off 16 bytes is refused
+    q = ctypes.c_void_p(0x100008)
+    assert L.agft_env_reset(cfg, p, n, p, p, q, None) == L.AGFT_E_INVAL
+    assert L.agft_env_step(cfg, p, n, 0, p, p, p, p, q, None) == L.AGFT_E_INVAL
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
