@@ -1,0 +1,44 @@
+"""bench.py end to end on the GPU: one short run and the fields of its JSON
+line (the contract the benchmark driver reads)."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_bench_json_line():
+    cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", "cfg2", "--steps", "30",
+           "--warmup", "3", "--cpu-budget", "1"]
+    print("[bench test]", " ".join(cmd[2:]), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=240, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    assert len(lines) == 1, r.stdout
+    d = json.loads(lines[0])
+    assert d["metric"].startswith("bandit decision-steps/sec")
+    assert d["unit"] == "decision-steps/s" and d["value"] > 0
+    assert d["n_gpus"] == 1 and d["steps"] == 30 and d["warmup"] == 3
+    assert d["higher_is_better"] is True and d["scaling"] == "weak" and d["vs_baseline"] is None
+    assert d["dtype"] == "f32" and d["data"].startswith("synthetic")
+    assert d["config"]["workload"].startswith("cfg2")
+    # throughput is B * steps over the timed region
+    assert abs(d["value"] - 4096 * 30 / (d["ms_per_step"] * 30 * 1e-3)) < 1e-6 * d["value"]
+    rf = d["roofline"]
+    assert rf["bound"] == "hbm" and rf["unit"] == "GB/s" and rf["peak"] == 8000.0
+    assert rf["achieved"] > 0 and abs(rf["frac"] - rf["achieved"] / rf["peak"]) < 1e-12
+    # the committed counters were taken on cfg4, so none are reported here
+    assert rf["traffic"] is None
+    det = d["detail"]
+    assert 0 < det["step_kernel_avg_ms"] < d["ms_per_step"]
+    assert abs(rf["achieved"] - det["algorithmic_bytes_per_launch"] / (det["step_kernel_avg_ms"] * 1e-3) / 1e9) \
+        < 1e-6 * rf["achieved"]
+    cb = d["cpu_baseline"]
+    assert cb["kind"] == "oracle" and cb["unit"] == "decision-steps/s" and cb["value"] > 0
+    assert cb["cores"] >= 1 and "cfg2" in cb["sample"]
+    assert det["cpu_oracle_1thread"]["cores"] == 1
