@@ -474,14 +474,21 @@ __device__ T block_reduce(T v, T *red, int lane, int wave, int nwave, Op op) {
     return out;
 }
 
-// Wavefronts per SIMD the register allocation must allow, by context dimension.
-template <int D>
+// Wavefronts per SIMD the register allocation must allow.  At d = 16 with
+// packed tails (instances that stream more than 16 KB, four wavefronts each)
+// the code the compiler gives at six (75 registers) beats the one squeezed
+// into seven (72): step kernel 842 vs 848 us at K=128 B=65,536, 211.7 vs
+// 212.8 us at B=16,384.  With padded tails (small streams, one wavefront
+// per instance, many instances in flight) seven wins: 173.6 vs 183.1 us
+// with the refinement, rules and switch, 48.6 vs 49.8 us with the
+// refinement alone.
+template <int D, int TF>
 struct Occupancy {
-    static constexpr int waves = D == 32 ? 4 : 7;
+    static constexpr int waves = D == 32 ? 4 : (D == 16 && TF == 3 ? 6 : 7);
 };
 
 template <int D, int TF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Occupancy<D>::waves)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Occupancy<D, TF>::waves)))
 void agft_step_kernel(StepArgs p) {
     using R = Rec<D, TF>;
     constexpr int G = R::G, S = R::S;
