@@ -474,21 +474,23 @@ __device__ T block_reduce(T v, T *red, int lane, int wave, int nwave, Op op) {
     return out;
 }
 
-// Wavefronts per SIMD the register allocation must allow.  At d = 16 with
-// packed tails (instances that stream more than 16 KB, four wavefronts each)
-// the code the compiler gives at six (75 registers) beats the one squeezed
-// into seven (72): step kernel 842 vs 848 us at K=128 B=65,536, 211.7 vs
-// 212.8 us at B=16,384.  With padded tails (small streams, one wavefront
-// per instance, many instances in flight) seven wins: 173.6 vs 183.1 us
-// with the refinement, rules and switch, 48.6 vs 49.8 us with the
-// refinement alone.
-template <int D, int TF>
-struct Occupancy {
-    static constexpr int waves = D == 32 ? 4 : (D == 16 && TF == 3 ? 6 : 7);
-};
+// Wavefronts per SIMD the register allocation must allow (the kernel's W).
+// At d = 16 with packed tails (instances that stream more than 16 KB, four
+// wavefronts each) the code the compiler gives at six (75 registers) beats
+// the one squeezed into seven (72): step kernel 842 vs 848 us at K=128
+// B=65,536, 211.7 vs 212.8 us at B=16,384.  Seven wins everywhere else:
+// with the paper's rules 2-8, whose pass over the arm statistics gains from
+// more instances in flight (918.6 vs 885.2 us at K=128 B=65,536, 186.4 vs
+// 177.8 us at B=16,384), and with padded tails (one wavefront per instance):
+// 173.6 vs 183.1 us with the refinement, rules and switch, 48.6 vs 49.8 us
+// with the refinement alone.
+int occupancy_for(const agft_config &c, int tail) {
+    if (c.d == 32) return 4;
+    return c.d == 16 && tail == 3 && !(c.prune_rule & 14) ? 6 : 7;
+}
 
-template <int D, int TF>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(Occupancy<D, TF>::waves)))
+template <int D, int TF, int W>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(W)))
 void agft_step_kernel(StepArgs p) {
     using R = Rec<D, TF>;
     constexpr int G = R::G, S = R::S;
@@ -1400,16 +1402,18 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     const bool packed_tails = tail_floats(c) == 3;
     switch (c.d) {
         case 8:
-            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<8, 3>), grid, block, lds, h->stream, p);
-            else hipLaunchKernelGGL((agft_step_kernel<8, 4>), grid, block, lds, h->stream, p);
+            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<8, 3, 7>), grid, block, lds, h->stream, p);
+            else hipLaunchKernelGGL((agft_step_kernel<8, 4, 7>), grid, block, lds, h->stream, p);
             break;
         case 16:
-            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<16, 3>), grid, block, lds, h->stream, p);
-            else hipLaunchKernelGGL((agft_step_kernel<16, 4>), grid, block, lds, h->stream, p);
+            if (packed_tails && occupancy_for(c, 3) == 6)
+                hipLaunchKernelGGL((agft_step_kernel<16, 3, 6>), grid, block, lds, h->stream, p);
+            else if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<16, 3, 7>), grid, block, lds, h->stream, p);
+            else hipLaunchKernelGGL((agft_step_kernel<16, 4, 7>), grid, block, lds, h->stream, p);
             break;
         case 32:
-            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<32, 3>), grid, block, lds, h->stream, p);
-            else hipLaunchKernelGGL((agft_step_kernel<32, 4>), grid, block, lds, h->stream, p);
+            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<32, 3, 4>), grid, block, lds, h->stream, p);
+            else hipLaunchKernelGGL((agft_step_kernel<32, 4, 4>), grid, block, lds, h->stream, p);
             break;
         default: return AGFT_E_UNSUPPORTED;
     }
