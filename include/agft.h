@@ -212,6 +212,26 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
 int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t *d_action,
               float *d_scores);
 
+/* How agft_step launches the step kernel for cfg (host-only, no device
+ * call): one workgroup per instance.  The four fields follow from the
+ * configuration alone: the bytes an exploring instance streams per step
+ * (arms in play times 4(d + d(d+1)/2)) choose the record layout, with the
+ * switch the bytes an exploiting instance streams choose the workgroup
+ * width, and d, the layout and the pruning rules choose the register target
+ * and where the update runs. */
+typedef struct agft_launch_shape {
+    int32_t waves;        /* wavefronts per workgroup: 1 up to 16 KB streamed per
+                             instance, 4 beyond */
+    int32_t simd_waves;   /* wavefronts per SIMD the kernel's registers allow */
+    int32_t tail_floats;  /* record layout, as agft_state_view.tail_floats */
+    int32_t early_update; /* 1: the rank-1 update runs while the stream's first pass
+                             is in flight; 0: after the stream */
+} agft_launch_shape;
+
+/* Fill *out for cfg.  AGFT_E_INVAL if cfg is invalid or out is NULL,
+ * AGFT_E_UNSUPPORTED for a context dimension other than 8, 16, 32. */
+int agft_launch_shape_for(const agft_config *cfg, agft_launch_shape *out);
+
 /* Fill *out with device pointers into the state and the handle's counters. */
 int agft_get_state(const agft_handle *h, agft_state_view *out);
 

@@ -51,10 +51,14 @@ class agft_env_config(ctypes.Structure):
                 ("mu", _f32 * 7), ("sd", _f32 * 7)]
 
 
+class agft_launch_shape(ctypes.Structure):
+    _fields_ = [("waves", _i32), ("simd_waves", _i32), ("tail_floats", _i32), ("early_update", _i32)]
+
+
 ABI_VERSION = 4   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
-            "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version",
+            "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version", "agft_launch_shape_for",
             "agft_env_state_bytes", "agft_env_reset", "agft_env_step"]
 
 _lib = None
@@ -88,6 +92,8 @@ def _declare(lib):
     lib.agft_strerror.argtypes = [ctypes.c_int]
     lib.agft_abi_version.restype = ctypes.c_int
     lib.agft_abi_version.argtypes = []
+    lib.agft_launch_shape_for.restype = ctypes.c_int
+    lib.agft_launch_shape_for.argtypes = [cfgp, ctypes.POINTER(agft_launch_shape)]
     lib.agft_env_state_bytes.restype = _sz
     lib.agft_env_state_bytes.argtypes = [envp]
     lib.agft_env_reset.restype = ctypes.c_int
@@ -158,6 +164,12 @@ def agft_strerror(code):
 
 def agft_abi_version():
     return lib().agft_abi_version()
+
+
+def agft_launch_shape_for(cfg):
+    shape = agft_launch_shape()
+    code = lib().agft_launch_shape_for(ctypes.byref(cfg), ctypes.byref(shape))
+    return code, shape
 
 
 def agft_env_state_bytes(cfg):

@@ -1395,18 +1395,20 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
-    const int waves = waves_for(c);
-    p.early_update = early_update(c) ? 1 : 0;
+    agft_launch_shape shape;
+    agft_launch_shape_for(&c, &shape);
+    const int waves = shape.waves;
+    p.early_update = shape.early_update;
     const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves));
     const size_t lds = step_lds_bytes(c.K);
-    const bool packed_tails = tail_floats(c) == 3;
+    const bool packed_tails = shape.tail_floats == 3;
     switch (c.d) {
         case 8:
             if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<8, 3, 7>), grid, block, lds, h->stream, p);
             else hipLaunchKernelGGL((agft_step_kernel<8, 4, 7>), grid, block, lds, h->stream, p);
             break;
         case 16:
-            if (packed_tails && occupancy_for(c, 3) == 6)
+            if (packed_tails && shape.simd_waves == 6)
                 hipLaunchKernelGGL((agft_step_kernel<16, 3, 6>), grid, block, lds, h->stream, p);
             else if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<16, 3, 7>), grid, block, lds, h->stream, p);
             else hipLaunchKernelGGL((agft_step_kernel<16, 4, 7>), grid, block, lds, h->stream, p);
@@ -1425,6 +1427,16 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     } else {
         h->pending = 0;
     }
+    return AGFT_OK;
+}
+
+int agft_launch_shape_for(const agft_config *cfg, agft_launch_shape *out) {
+    if (out == nullptr || !config_ok(cfg)) return AGFT_E_INVAL;
+    if (!dim_supported(cfg->d)) return AGFT_E_UNSUPPORTED;
+    out->waves = waves_for(*cfg);
+    out->tail_floats = tail_floats(*cfg);
+    out->simd_waves = occupancy_for(*cfg, out->tail_floats);
+    out->early_update = early_update(*cfg) ? 1 : 0;
     return AGFT_OK;
 }
 

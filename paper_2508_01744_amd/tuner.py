@@ -15,6 +15,40 @@ def _stream_handle(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def make_config(B, K, d, lam=1.0, alpha0=1.0, alpha_sched=0, prune_rule=0, prune_period=50,
+                adopt=False, heuristics=None, exploit=None, refine=None):
+    """The agft_config of a tuner (no device work)."""
+    cfg = L.agft_config(int(B), int(K), int(d), float(lam), float(alpha0), int(alpha_sched),
+                        int(prune_rule), int(prune_period), L.AGFT_ADOPT_STATE if adopt else 0)
+    for name, value in (heuristics or {}).items():
+        setattr(cfg, name, value)
+    if exploit:
+        cfg.exploit = 1
+        for name, value in exploit.items():
+            setattr(cfg, name, value)
+    if refine:
+        cfg.refine = 1
+        for name, value in refine.items():
+            setattr(cfg, name, value)
+    return cfg
+
+
+def workload_config(wl, B=None):
+    """The agft_config of a workload from agft_workloads."""
+    return make_config(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0, wl.alpha_sched,
+                       wl.prune, wl.period, heuristics=wl.heuristics(),
+                       exploit=wl.page_hinkley() if wl.exploit else None,
+                       refine=wl.refinement() if wl.refine else None)
+
+
+def launch_shape(cfg):
+    """How agft_step launches the step kernel for cfg: dict(waves,
+    simd_waves, tail_floats, early_update)."""
+    code, shape = L.agft_launch_shape_for(cfg)
+    L.check("agft_launch_shape_for", code)
+    return {name: int(getattr(shape, name)) for name, _ in shape._fields_}
+
+
 class Tuner:
     """B independent AGFT frequency tuners (disjoint LinUCB over K arms, Sec. 4.2)."""
 
@@ -24,19 +58,8 @@ class Tuner:
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
-        self.cfg = L.agft_config(int(B), int(K), int(d), float(lam), float(alpha0),
-                                 int(alpha_sched), int(prune_rule), int(prune_period),
-                                 L.AGFT_ADOPT_STATE if adopt else 0)
-        for name, value in (heuristics or {}).items():
-            setattr(self.cfg, name, value)
-        if exploit:
-            self.cfg.exploit = 1
-            for name, value in exploit.items():
-                setattr(self.cfg, name, value)
-        if refine:
-            self.cfg.refine = 1
-            for name, value in refine.items():
-                setattr(self.cfg, name, value)
+        self.cfg = make_config(B, K, d, lam, alpha0, alpha_sched, prune_rule, prune_period, adopt,
+                               heuristics, exploit, refine)
         self.nbytes = L.agft_state_bytes(self.cfg)
         if self.nbytes == 0:
             raise ValueError("invalid tuner configuration")
