@@ -105,7 +105,7 @@ def step_bytes(wl, scored_exploring, scored_greedy, mask_write, update):
 
     Per instance: the previous decision's arm is read and written back once
     (its model: the d(d+1)/2 factor entries and theta, with its reward count
-    and sum); every other arm scored is read once, as its whole model while
+    and sum when a rule reads those); every other arm scored is read once, as its whole model while
     the instance explores (Eq. 1) and as theta alone once it exploits (Eq. 2);
     plus context, stashed context, reward, action and bookkeeping words, the
     per-arm reward statistics when the paper's rules 2-8 are on, the
@@ -117,7 +117,8 @@ def step_bytes(wl, scored_exploring, scored_greedy, mask_write, update):
     s = record_floats(d)
     kw = (wl.K + 31) // 32
     upd = B if update else 0
-    records = 4 * s * (scored_exploring + 2 * upd) + 4 * d * scored_greedy + 16 * upd
+    stats_kept = bool(wl.prune & 14) or bool(wl.refine)
+    records = 4 * s * (scored_exploring + 2 * upd) + 4 * d * scored_greedy + (16 * upd if stats_kept else 0)
     io = B * 4 * (3 * d + 7)           # ctx, xprev r/w; reward, action, aprev r/w, kact, bad
     if wl.prune & 14:
         io += B * 8 * wl.K             # per-arm count and reward sum

@@ -100,7 +100,7 @@ typedef struct agft_config {
        ph_window rounds, the instance exploits for good: a_t = argmax over the
        active arms of theta_k^T x_t (reported as both UCB and LCB), reading only
        the contiguous copy of theta that the state holds when this is on (4*d
-       bytes per arm, against 2*d*(d+4) for a whole record); rule 1 is not
+       bytes per arm, against 4*(d + d(d+1)/2) for a whole record); rule 1 is not
        applied; updates go on.  A buffer adopted with AGFT_ADOPT_STATE must have
        been made with the same setting. */
     int32_t exploit;
@@ -170,7 +170,9 @@ typedef struct agft_state_view {
                            [16 .. 16+d) context of the last decision (fp32) */
     int32_t inst_words; /* words per instance block: 16 + d rounded up to 16 */
     int32_t *stats;     /* [B][K][2] per arm: [0] rewards folded in (int32),
-                           [1] their sum (fp32 bits) */
+                           [1] their sum (fp32 bits).  Maintained only when a rule
+                           that reads them is on (prune_rule bits 2, 4, 8, or
+                           refine); otherwise they stay 0. */
     float *theta;       /* [B][K][d] copy of theta_k (Eq. 5), kept in step with the
                            records, which exploiting instances read in their place;
                            NULL when cfg.exploit is 0 */
@@ -187,7 +189,9 @@ size_t agft_state_bytes(const agft_config *cfg);
  * 256-byte aligned) and HIP stream (a hipStream_t; NULL = the null stream).
  * Without AGFT_ADOPT_STATE, enqueues the initialisation: S_k = I / sqrt(lambda),
  * theta_k = 0, every arm active, t = 0.  With it, reads the buffer's header
- * back (synchronously) and resumes from its t; the header must match cfg.
+ * back (synchronously) and resumes from its t; the header must match cfg
+ * (dimensions, record layout, the switch, and whether the per-arm reward
+ * statistics are maintained), else AGFT_E_STATE.
  * *out receives the handle; on error *out is set to NULL.
  */
 int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stream,

@@ -71,7 +71,8 @@ struct alignas(16) StateHeader {
     int32_t alpha_sched, prune_rule, prune_period;
     int32_t exploit;      // 1: the buffer holds the theta copy of the switch
     int32_t tail_floats;  // record layout: floats per lane slice of a tail
-    uint32_t reserved[45];
+    int32_t stats_kept;   // 1: the per-arm reward counts and sums are maintained
+    uint32_t reserved[44];
 };
 static_assert(sizeof(StateHeader) == 256, "header is 256 bytes");
 
@@ -218,6 +219,12 @@ size_t explore_bytes(const agft_config &c) {
 // and the switch 190 / 179 us.
 int tail_floats(const agft_config &c) { return explore_bytes(c) > 16384 ? 3 : 4; }
 
+// The per-arm reward counts and sums are read only by the paper's rules 2-8
+// and by the refinement's statistical anchor; without those the update
+// skips them (their one-line store per instance and step costs 1.4% of the
+// step at K=128 d=16 B=65,536) and they stay at zero.
+bool stats_kept(const agft_config &c) { return (c.prune_rule & 14) != 0 || c.refine != 0; }
+
 // theta copy [B][K][d] only with the switch to exploitation (0 bytes otherwise)
 Layout layout_for(const agft_config &c) {
     Layout L;
@@ -359,6 +366,7 @@ struct StepArgs {
     int32_t apply_update;  // a decision is pending
     int32_t prune_now;
     int32_t early_update;  // fold the previous reward in before the stream
+    int32_t keep_stats;    // maintain the per-arm reward counts and sums
     float alpha;
     int64_t t_next;        // t after this call (header bookkeeping)
 };
@@ -618,7 +626,7 @@ void agft_step_kernel(StepArgs p) {
                 cmap[q] = ld_chunk_map<D, TF>(c);
             }
         }
-        if (tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
+        if (p.keep_stats && tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
     }
 
     // the arms in play: not removed by a pruning rule, inside the action space
@@ -869,7 +877,7 @@ void agft_step_kernel(StepArgs p) {
                 float4 *tdst = reinterpret_cast<float4 *>(p.theta + ((size_t)inst * K + a_upd) * D);
                 tdst[tid] = make_float4(s_new[4 * tid], s_new[4 * tid + 1], s_new[4 * tid + 2], s_new[4 * tid + 3]);
             }
-            if (tid == 0)
+            if (p.keep_stats && tid == 0)
                 p.stats[(size_t)inst * K + a_upd] =
                     make_int2(s_stu.x + 1, __float_as_int(__int_as_float(s_stu.y) + r));
         } else if (has_prev && tid == 0) {
@@ -1258,6 +1266,7 @@ StateHeader make_header(const agft_config *c) {
     h.d = c->d;
     h.chunks = chunks_for(c->d, tail_floats(*c));
     h.tail_floats = tail_floats(*c);
+    h.stats_kept = stats_kept(*c) ? 1 : 0;
     h.mask_words = (c->K + 31) / 32;
     h.pending = 0;
     h.t = 0;
@@ -1311,6 +1320,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
         }
         if (got.magic != kMagic || got.version != want.version || got.B != want.B || got.K != want.K ||
             got.d != want.d || got.chunks != want.chunks || got.tail_floats != want.tail_floats ||
+            got.stats_kept != want.stats_kept ||
             got.exploit != want.exploit || got.t < 0 ||
             (got.pending != 0 && got.pending != 1)) {
             delete h;
@@ -1399,6 +1409,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     agft_launch_shape_for(&c, &shape);
     const int waves = shape.waves;
     p.early_update = shape.early_update;
+    p.keep_stats = stats_kept(c) ? 1 : 0;
     const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves));
     const size_t lds = step_lds_bytes(c.K);
     const bool packed_tails = shape.tail_floats == 3;

@@ -25,7 +25,6 @@ def test_step_bytes_worked_cases():
     wl = get_workload("cfg4")
     B = wl.B
     per_inst = (4 * 152 * (127 + 2)     # 127 other arms read, the updated arm read and written
-                + 16                    # its reward count and sum, read and written
                 + 4 * (3 * 16 + 7)      # context, stashed context, words
                 + 4 * 4)                # mask words read
     assert bench.step_bytes(wl, 127 * B, 0, False, True) == B * per_inst
@@ -34,10 +33,11 @@ def test_step_bytes_worked_cases():
     # an exploiting instance reads theta alone: 64 bytes per arm at d = 16
     assert (bench.step_bytes(wl, 0, 127 * B, False, True) - bench.step_bytes(wl, 0, 0, False, True)
             == B * 127 * 64)
-    # the paper's rules add the per-arm statistics; the switch its test words
+    # the paper's rules add the per-arm statistics (read by the rules, and the
+    # updated arm's count and sum kept); the switch its test words
     wp, we = get_workload("cfg4p"), get_workload("cfg4e")
     base = bench.step_bytes(wl, 0, 0, False, True)
-    assert bench.step_bytes(wp, 0, 0, False, True) - base == B * 8 * 128
+    assert bench.step_bytes(wp, 0, 0, False, True) - base == B * (8 * 128 + 16)
     assert bench.step_bytes(we, 0, 0, False, True) - base == B * 72
 
 

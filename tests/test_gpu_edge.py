@@ -72,9 +72,14 @@ def test_untouched_arms_are_swept_in_order():
     assert (a == np.arange(K)[:, None]).all()
 
 
+RULES = dict(ext_rounds=60, ext_min_n=3, ext_thr=-1.2, hist_after=30, hist_min_n=6, hist_kappa=1.0,
+             hist_min_arms=3, cascade_k=0)
+
+
 def test_missing_reward_and_flush():
     dev = torch.device("cuda")
-    tuner = Tuner(4, 16, 8, device=dev)
+    # rule bit 4 on, so that the per-arm reward statistics are kept
+    tuner = Tuner(4, 16, 8, prune_rule=4, device=dev, heuristics=RULES)
     X, R = random_contexts(6, 3, 4, 8)
     x = torch.as_tensor(X, dtype=torch.float32, device=dev)
     r = torch.as_tensor(R, dtype=torch.float32, device=dev)
@@ -91,6 +96,27 @@ def test_missing_reward_and_flush():
     tuner.step(x[2])          # no reward needed after a flush
     torch.cuda.synchronize()
     assert tuner.t == 3
+
+
+def test_statistics_only_kept_when_read():
+    """Without rules 2-8 or the refinement nothing reads the per-arm reward
+    statistics: they stay zero, and a buffer made so cannot be adopted by a
+    configuration that reads them."""
+    dev = torch.device("cuda")
+    X, R = random_contexts(7, 3, 4, 8)
+    x = torch.as_tensor(X, dtype=torch.float32, device=dev)
+    r = torch.as_tensor(R, dtype=torch.float32, device=dev)
+    tuner = Tuner(4, 16, 8, device=dev)
+    tuner.step(x[0])
+    tuner.step(x[1], r[0])
+    tuner.flush(r[1])
+    torch.cuda.synchronize()
+    assert int(tuner.view()["stats"].abs().sum()) == 0
+    state = tuner.state.clone()
+    tuner.close()
+    with pytest.raises(AgftError) as e:
+        Tuner(4, 16, 8, prune_rule=4, device=dev, heuristics=RULES, state=state, adopt=True)
+    assert e.value.code == L.AGFT_E_STATE
 
 
 def test_non_finite_inputs():
