@@ -11,7 +11,7 @@ Environment constants (power/latency closed form, feature normalisation) are
 data: both the GPU simulator and the CPU oracle read them from here and each
 implements the closed form on its own.
 """
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 import math
 
 

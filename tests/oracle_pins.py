@@ -12,7 +12,6 @@ squares, an exact rational hand derivation, explicit loops for argmax and
 pruning, and statistical convergence on a known linear reward.
 """
 import math
-from fractions import Fraction
 
 import numpy as np
 

@@ -3,7 +3,6 @@
 Small cases record every instance at every step; full-size cases run the
 whole batch at the benchmark's launch configuration and record 64 probe
 instances (strided, first and last) at every step."""
-import numpy as np
 import pytest
 import torch
 

@@ -6,7 +6,6 @@ the switch to exploitation.
 Open loop (the same contexts and rewards to both sides) with short refinement
 periods so that windows move often; closed loop on the workloads with the
 refinement enabled."""
-import numpy as np
 import pytest
 import torch
 

@@ -1,7 +1,6 @@
 """Plant plausible mistakes in a copy of the oracle (CPU only) and check that
 the pins catch every one.  The planted copies are compiled into a temporary
 directory; the real oracle is untouched."""
-import os
 
 import pytest
 
