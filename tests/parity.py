@@ -238,6 +238,112 @@ class Checker:
         return self.st
 
 
+class EveryInstanceChecker:
+    """The comparison of Checker for runs recorded without scores, vectorised
+    over instances so that it covers every instance of a full-size batch:
+    contexts, rewards, prune decisions and actions at every step, under the
+    same near-tie rules (where the oracle's fp64 scores leave the choice
+    open, it adopts the GPU's).  For the workloads without the paper's
+    rules, the switch or the refinement.
+
+    g_a [T][n] actions, g_words [T][n][KW] mask words after each step,
+    g_x [T][n][d] contexts and g_r [T][n] rewards (reward of decision t)."""
+
+    def __init__(self, name, K, ids, g_a, g_words, g_x, g_r):
+        self.name, self.K, self.ids = name, K, np.asarray(ids)
+        self.g_a, self.g_words, self.g_x, self.g_r = g_a, g_words, g_x, g_r
+        self.st = dict(max_ctx_err=0.0, max_reward_err=0.0, forced=0, forced_prune=0,
+                       exact_tie_steps=0, decisions=0, no_decision=0, instances=len(self.ids))
+
+    def fail(self, msg):
+        raise ParityError(f"{self.name}: {msg}")
+
+    def __call__(self, t, x, r_prev, ucb, lcb, keep, action):
+        st, K = self.st, self.K
+        gx = np.asarray(self.g_x[t], dtype=np.float64)
+        with np.errstate(invalid="ignore"):
+            ex = np.where(np.isfinite(x), np.abs(gx - x) / np.maximum(1.0, np.abs(x)), 0.0)
+        st["max_ctx_err"] = max(st["max_ctx_err"], float(ex.max()))
+        if ex.max() > ENV_TOL:
+            i = int(np.argmax(ex.max(axis=1)))
+            self.fail(f"context mismatch at t={t}, instance {self.ids[i]}: {gx[i]} vs {x[i]}")
+        if t > 0:
+            gr = np.asarray(self.g_r[t - 1], dtype=np.float64)
+            er = np.abs(gr - r_prev) / np.maximum(1.0, np.abs(r_prev))
+            st["max_reward_err"] = max(st["max_reward_err"], float(er.max()))
+            if er.max() > ENV_TOL:
+                i = int(np.argmax(er))
+                self.fail(f"reward mismatch at t={t - 1}, instance {self.ids[i]}: {gr[i]} vs {r_prev[i]}")
+        ga = np.asarray(self.g_a[t], dtype=np.int64)
+        dec = action >= 0
+        st["no_decision"] += int((~dec).sum())
+        if np.any(~dec & (ga != -1)):
+            i = int(np.flatnonzero(~dec & (ga != -1))[0])
+            self.fail(f"GPU decided on a non-finite context at t={t}, instance {self.ids[i]}")
+        act = np.isfinite(ucb)
+        g_keep = mask_words_to_bool(self.g_words[t], K)
+        commit_keep = keep.copy()
+        diff = (g_keep != keep) & dec[:, None]
+        rows = np.flatnonzero(diff.any(axis=1))
+        if rows.size:
+            # a prune decision may differ only where the arm's UCB is within
+            # TIE of the largest LCB over the active arms
+            lstar = np.where(act[rows], lcb[rows], -np.inf).max(axis=1)
+            amb = np.abs(ucb[rows] - lstar[:, None]) <= TIE * np.maximum(1.0, np.abs(lstar))[:, None]
+            bad = diff[rows] & ~amb
+            if bad.any():
+                q = int(np.flatnonzero(bad.any(axis=1))[0])
+                self.fail(f"prune mismatch at t={t}, instance {self.ids[rows[q]]}, "
+                          f"arms {np.flatnonzero(bad[q])}")
+            commit_keep[rows] = g_keep[rows]
+            st["forced_prune"] += int(rows.size)
+        u = np.where(commit_keep, ucb, -np.inf)
+        ustar = u.max(axis=1)
+        own = u.argmax(axis=1)          # the lowest index among exact maxima
+        tol = TIE * np.maximum(1.0, np.abs(ustar))
+        with np.errstate(invalid="ignore"):
+            near = commit_keep & ((ustar[:, None] - ucb) <= tol[:, None])
+        valid = (ga >= 0) & (ga < K)
+        gac = np.clip(ga, 0, K - 1)
+        ok = ~dec | (valid & near[np.arange(len(ga)), gac])
+        if not ok.all():
+            i = int(np.flatnonzero(~ok)[0])
+            gu = ucb[i, ga[i]] if valid[i] else None
+            self.fail(f"action mismatch at t={t}, instance {self.ids[i]}: GPU {ga[i]} (UCB {gu}), "
+                      f"oracle {own[i]} (UCB {ustar[i]})")
+        # exact ties (every near arm bit-identical to the best): lowest index on both sides
+        exact = dec & (near.sum(axis=1) > 1) & np.all(~near | (ucb == ustar[:, None]), axis=1)
+        wrong = exact & (ga != own)
+        if wrong.any():
+            i = int(np.flatnonzero(wrong)[0])
+            self.fail(f"exact tie broken wrongly at t={t}, instance {self.ids[i]}: {ga[i]} vs {own[i]}")
+        st["exact_tie_steps"] += int(exact.sum())
+        st["forced"] += int((dec & (ga != own)).sum())
+        st["decisions"] += int(dec.sum())
+        return np.where(dec, ga, action).astype(np.int32), commit_keep
+
+    def finish(self):
+        self.st["forced_rate"] = self.st["forced"] / max(1, self.st["decisions"])
+        return self.st
+
+
+def compare_every_instance(wl, T, rec, ids):
+    """Closed loop without scores: replay instances ids (any subset of the
+    batch, in order) through the oracle and its environment and compare each
+    one's contexts, rewards, prune decisions and actions at every step; raise
+    ParityError on a violation.  rec: host arrays recorded for those
+    instances, a [T][n], mask [T][n][KW], x [T][n][d], r [T][n] (the probe
+    records of paper_2508_01744_amd.run_closed_loop)."""
+    ids = np.asarray(ids)
+    arrivals, noise = exogenous(wl, ids, T)
+    chk = EveryInstanceChecker(wl.name, wl.K, ids, np.asarray(rec["a"]), np.asarray(rec["mask"]),
+                               np.asarray(rec["x"]), np.asarray(rec["r"]))
+    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk)
+    st = chk.finish()
+    st["oracle"] = out["oracle"]
+    return st
+
+
 def compare(wl, T, probes, rec):
     """Closed loop: replay the probe instances through the oracle and its
     environment; raise ParityError on a violation.  rec: host tensors from

@@ -1,0 +1,38 @@
+"""The four batched workloads at full size, in the benchmark's launch
+configuration, compared with the fp64 oracle on far more instances than the
+score probes of the full-size parity tests: every instance of cfg2 (4,096)
+and cfg5 (1,024), every fourth of cfg3 and every sixteenth of cfg4 (4,096
+each, the last instance included), closed loop, at every step: contexts,
+rewards, prune decisions and actions (identical except at near-ties), then
+the final models.  (cfg1 is a single instance, compared in full by the
+parity tests.)"""
+import pytest
+import torch
+
+import parity
+from agft_workloads import ENV, exogenous, get_workload
+from gpu_helpers import compare_model, say
+from paper_2508_01744_amd import run_closed_loop
+
+pytestmark = pytest.mark.gpu
+
+STRIDE = {"cfg2": 1, "cfg3": 4, "cfg4": 16, "cfg5": 1}
+
+
+@pytest.mark.parametrize("name", sorted(STRIDE))
+def test_many_instances_full_size(name):
+    wl = get_workload(name)
+    ids = list(range(0, wl.B, STRIDE[name]))
+    if ids[-1] != wl.B - 1:
+        ids.append(wl.B - 1)
+    say(f"[every] {wl.name} B={wl.B} K={wl.K} d={wl.d} T={wl.T}: {len(ids)} instances compared")
+    arr, noi = exogenous(wl)
+    out = run_closed_loop(wl, ENV, arr, noi, probes=ids)
+    rec = {k: out["probes"][k].numpy() for k in ("a", "mask", "x", "r")}
+    st = parity.compare_every_instance(wl, wl.T, rec, ids)
+    wth, wai = compare_model(out["tuner"], st["oracle"], ids, 1e-3, 1e-4)
+    say(f"[every] {wl.name}: {st['decisions']} decisions, forced {st['forced']}, prune forced "
+        f"{st['forced_prune']}, exact-tie steps {st['exact_tie_steps']}, ctx err {st['max_ctx_err']:.2e}, "
+        f"reward err {st['max_reward_err']:.2e}, theta err {wth:.2e}, Ainv err {wai:.2e}")
+    del out
+    torch.cuda.empty_cache()

@@ -114,3 +114,75 @@ def test_planted_window_difference_fails(plant):
         win[t:, 2, 2] = RCFG["refine"]["refine_stride"]
     with pytest.raises(parity.ParityError):
         parity.compare_open_loop("planted-window", RCFG, X, R, a, m, s, g_win=win)
+
+
+# ---- the vectorised every-instance comparison (closed loop, no scores) ----
+
+def _closed_record(wl):
+    """The oracle's own closed-loop run, kept in the GPU run's formats."""
+    from agft_workloads import exogenous
+    from oracle import run_closed_loop
+    arrivals, noise = exogenous(wl, None, wl.T)
+    out = run_closed_loop(wl, arrivals, noise, T=wl.T, record=True)
+    T, n, K = out["keep"].shape
+    words = np.zeros((T, n, (K + 31) // 32), np.int64)
+    for k in range(K):
+        words[:, :, k // 32] |= out["keep"][:, :, k].astype(np.int64) << (k % 32)
+    rec = dict(a=out["actions"].copy(), mask=words.astype(np.uint32).view(np.int32),
+               x=out["x"].astype(np.float32), r=out["r"].astype(np.float32))
+    return rec, out
+
+
+def _wl():
+    from agft_workloads import get_workload
+    return get_workload(3, B=6, K=24, T=120)
+
+
+def test_every_instance_oracle_record_passes():
+    wl = _wl()
+    rec, out = _closed_record(wl)
+    assert not out["keep"][-1].all()   # pruning happened
+    st = parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
+    assert st["decisions"] == wl.B * wl.T and st["forced"] == 0 and st["forced_prune"] == 0
+    assert st["exact_tie_steps"] > 0   # untouched arms at the start
+    # any subset of the batch, in order
+    sub = [1, 4]
+    st = parity.compare_every_instance(wl, wl.T, {k: v[:, sub] for k, v in rec.items()}, sub)
+    assert st["decisions"] == 2 * wl.T
+
+
+@pytest.mark.parametrize("plant", ["action", "context", "reward", "prune", "exact_tie"])
+def test_every_instance_planted_difference_fails(plant):
+    wl = _wl()
+    rec, out = _closed_record(wl)
+    ucb, keep = out["ucb"], out["keep"]
+    if plant == "action":
+        # the second-best arm where the top two are far apart
+        u = np.where(keep, ucb, -np.inf)
+        top = np.sort(u, axis=2)
+        gap = top[..., -1] - top[..., -2]
+        t, i = map(int, np.argwhere(gap[60:] > 1e-2)[0])
+        t += 60
+        rec["a"][t, i] = int(np.argsort(u[t, i])[-2])
+    elif plant == "context":
+        rec["x"][70, 2, 3] += 1e-3
+    elif plant == "reward":
+        rec["r"][70, 3] += 1e-3
+    elif plant == "prune":
+        # an arm far above the threshold dropped at the prune step
+        t = wl.period
+        i = 0
+        lstar = np.where(np.isfinite(ucb[t, i]), out["lcb"][t, i], -np.inf).max()
+        k = int(np.flatnonzero(keep[t, i] & (ucb[t, i] - lstar > 1e-2))[0])
+        if k == int(rec["a"][t, i]):
+            k = int(np.flatnonzero(keep[t, i] & (ucb[t, i] - lstar > 1e-2))[1])
+        words = rec["mask"].view(np.uint32)
+        words[t:, i, k // 32] &= np.uint32(0xFFFFFFFF ^ (1 << (k % 32)))
+    else:
+        # step 0: every arm untouched and bit-identical; the lowest index must win
+        assert (ucb[0, 0] == ucb[0, 0, 0]).all()
+        rec["a"][0, 0] = 1
+    expect = {"action": "action mismatch", "context": "context mismatch", "reward": "reward mismatch",
+              "prune": "prune mismatch", "exact_tie": "exact tie"}[plant]
+    with pytest.raises(parity.ParityError, match=expect):
+        parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
