@@ -896,18 +896,32 @@ void agft_step_kernel(StepArgs p) {
         const float x0 = pick<D>(x, 4 * jt), x1 = pick<D>(x, 4 * jt + 1);
         const float x2 = pick<D>(x, 4 * jt + 2), x3 = pick<D>(x, 4 * jt + 3);
         const float4 *th = reinterpret_cast<const float4 *>(p.theta + (size_t)inst * K * D);
-        for (int base = 0; base < nlist; base += apt) {
-            const int slot = base + gt;
-            const int k_cur = slot < nlist ? s_list[slot] : -1;
-            float m = 0.0f;
-            if (k_cur >= 0) {
-                const float4 v = ld_nt(th + (size_t)k_cur * GT + jt);
-                m = fmaf(v.w, x3, fmaf(v.z, x2, fmaf(v.y, x1, v.x * x0)));
+        // UT passes' loads are issued before any of them is used, so that an
+        // instance waits for about one load latency per UT passes (three at
+        // d = 16 with seven wavefronts per SIMD, where four would spill).
+        // The explicit wait first (gfx9 encoding: vmcnt 0 only) clears the
+        // loads of the prologue, all consumed by now, from the compiler's
+        // count: otherwise a register they targeted, reused in the loop,
+        // would make it wait for every load in flight in each pass.
+        constexpr int UT = D == 16 && W >= 7 ? 3 : 4;
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        for (int base = 0; base < nlist; base += UT * apt) {
+            int kc[UT];
+            float4 v[UT];
+#pragma unroll
+            for (int u = 0; u < UT; ++u) {
+                const int slot = base + u * apt + gt;
+                kc[u] = slot < nlist ? s_list[slot] : -1;
+                v[u] = kc[u] >= 0 ? ld_nt(th + (size_t)kc[u] * GT + jt) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
             }
-            m = group_sum<GT>(m);
-            if (k_cur >= 0 && jt == 0) {
-                s_ucb[k_cur] = m;
-                s_lcb[k_cur] = m;
+#pragma unroll
+            for (int u = 0; u < UT; ++u) {
+                float m = kc[u] >= 0 ? fmaf(v[u].w, x3, fmaf(v[u].z, x2, fmaf(v[u].y, x1, v[u].x * x0))) : 0.0f;
+                m = group_sum<GT>(m);
+                if (kc[u] >= 0 && jt == 0) {
+                    s_ucb[kc[u]] = m;
+                    s_lcb[kc[u]] = m;
+                }
             }
         }
     } else {
