@@ -5,7 +5,14 @@ and cfg5 (1,024), every fourth of cfg3 and every sixteenth of cfg4 (4,096
 each, the last instance included), closed loop, at every step: contexts,
 rewards, prune decisions and actions (identical except at near-ties), then
 the final models.  (cfg1 is a single instance, compared in full by the
-parity tests.)"""
+parity tests.)
+
+With AGFT_EVERY_INSTANCE=1, every instance of cfg3 (16,384) and cfg4 (65,536)
+as well, in parts that share one GPU run per workload (minutes of oracle time
+on the host, so not part of the default run)."""
+import os
+
+import numpy as np
 import pytest
 import torch
 
@@ -36,3 +43,39 @@ def test_many_instances_full_size(name):
         f"reward err {st['max_reward_err']:.2e}, theta err {wth:.2e}, Ainv err {wai:.2e}")
     del out
     torch.cuda.empty_cache()
+
+
+PARTS = {"cfg3": 2, "cfg4": 4}
+_runs = {}
+
+
+def _gpu_run(name):
+    """One full-size run per workload, every instance recorded (host copies)."""
+    if name not in _runs:
+        _runs.clear()
+        torch.cuda.empty_cache()
+        wl = get_workload(name)
+        arr, noi = exogenous(wl)
+        out = run_closed_loop(wl, ENV, arr, noi, probes=range(wl.B))
+        rec = {k: out["probes"][k].numpy() for k in ("a", "mask", "x", "r")}
+        _runs[name] = (wl, rec, out["tuner"])
+    return _runs[name]
+
+
+@pytest.mark.skipif(os.environ.get("AGFT_EVERY_INSTANCE") != "1",
+                    reason="every instance of cfg3 and cfg4 takes minutes of oracle time; "
+                           "set AGFT_EVERY_INSTANCE=1")
+@pytest.mark.parametrize("name,part", [(w, q) for w in sorted(PARTS) for q in range(PARTS[w])])
+def test_every_instance_full_size(name, part):
+    wl, rec, tuner = _gpu_run(name)
+    n = wl.B // PARTS[name]
+    ids = np.arange(part * n, (part + 1) * n)
+    say(f"[every-all] {wl.name}: instances {ids[0]}..{ids[-1]}")
+    st = parity.compare_every_instance(wl, wl.T, {k: v[:, ids] for k, v in rec.items()}, ids)
+    wth, wai = compare_model(tuner, st["oracle"], ids, 1e-3, 1e-4)
+    say(f"[every-all] {wl.name} part {part}: {st['decisions']} decisions, forced {st['forced']}, prune forced "
+        f"{st['forced_prune']}, exact-tie steps {st['exact_tie_steps']}, ctx err {st['max_ctx_err']:.2e}, "
+        f"reward err {st['max_reward_err']:.2e}, theta err {wth:.2e}, Ainv err {wai:.2e}")
+    if part == PARTS[name] - 1:
+        _runs.clear()
+        torch.cuda.empty_cache()
