@@ -243,22 +243,36 @@ class EveryInstanceChecker:
     over instances so that it covers every instance of a full-size batch:
     contexts, rewards, prune decisions and actions at every step, under the
     same near-tie rules (where the oracle's fp64 scores leave the choice
-    open, it adopts the GPU's).  For the workloads without the paper's
-    rules, the switch or the refinement.
+    open, it adopts the GPU's).  With the paper's rules (bits 2, 4, 8) an
+    arm may also be kept or removed differently when its rule comparison, or
+    that of a higher arm whose cascade covers it, sat within TIE of the
+    threshold; the oracle then adopts the GPU's active set and action.  For
+    the workloads without the switch or the refinement.
 
     g_a [T][n] actions, g_words [T][n][KW] mask words after each step,
     g_x [T][n][d] contexts and g_r [T][n] rewards (reward of decision t)."""
 
-    def __init__(self, name, K, ids, g_a, g_words, g_x, g_r):
+    def __init__(self, name, K, ids, g_a, g_words, g_x, g_r, rules=0, cascade_k=0):
         self.name, self.K, self.ids = name, K, np.asarray(ids)
         self.g_a, self.g_words, self.g_x, self.g_r = g_a, g_words, g_x, g_r
-        self.st = dict(max_ctx_err=0.0, max_reward_err=0.0, forced=0, forced_prune=0,
+        self.rules, self.cascade_k = rules, cascade_k
+        self.st = dict(max_ctx_err=0.0, max_reward_err=0.0, forced=0, forced_prune=0, forced_rules=0,
                        exact_tie_steps=0, decisions=0, no_decision=0, instances=len(self.ids))
+
+    def _rules_ambiguous(self, margins):
+        """[n][K]: arm k's removal by rules 2/4/8 could go either way."""
+        amb = margins <= TIE
+        if self.rules & 8:
+            arms = np.arange(self.K)
+            cand = amb & (arms < self.cascade_k)
+            top = np.where(cand.any(axis=1), self.K - 1 - np.argmax(cand[:, ::-1], axis=1), -1)
+            amb = amb | (arms[None, :] < top[:, None])
+        return amb
 
     def fail(self, msg):
         raise ParityError(f"{self.name}: {msg}")
 
-    def __call__(self, t, x, r_prev, ucb, lcb, keep, action):
+    def __call__(self, t, x, r_prev, ucb, lcb, keep, action, margins=None):
         st, K = self.st, self.K
         gx = np.asarray(self.g_x[t], dtype=np.float64)
         with np.errstate(invalid="ignore"):
@@ -285,18 +299,27 @@ class EveryInstanceChecker:
         commit_keep = keep.copy()
         diff = (g_keep != keep) & dec[:, None]
         rows = np.flatnonzero(diff.any(axis=1))
+        by_rules = np.zeros(len(ga), dtype=bool)
         if rows.size:
             # a prune decision may differ only where the arm's UCB is within
-            # TIE of the largest LCB over the active arms
+            # TIE of the largest LCB over the active arms (rule 1), or where
+            # the paper's rules could go either way
             lstar = np.where(act[rows], lcb[rows], -np.inf).max(axis=1)
-            amb = np.abs(ucb[rows] - lstar[:, None]) <= TIE * np.maximum(1.0, np.abs(lstar))[:, None]
-            bad = diff[rows] & ~amb
+            with np.errstate(invalid="ignore"):
+                amb1 = np.abs(ucb[rows] - lstar[:, None]) <= TIE * np.maximum(1.0, np.abs(lstar))[:, None]
+            amb_r = (self._rules_ambiguous(margins[rows]) if margins is not None
+                     else np.zeros_like(amb1))
+            bad = diff[rows] & ~(amb1 | amb_r)
             if bad.any():
                 q = int(np.flatnonzero(bad.any(axis=1))[0])
                 self.fail(f"prune mismatch at t={t}, instance {self.ids[rows[q]]}, "
                           f"arms {np.flatnonzero(bad[q])}")
             commit_keep[rows] = g_keep[rows]
-            st["forced_prune"] += int(rows.size)
+            # where a rule decided differently the two sides scored different
+            # sets: the GPU's decision is taken as it is
+            by_rules[rows] = (diff[rows] & amb_r & ~amb1).any(axis=1)
+            st["forced_rules"] += int(by_rules.sum())
+            st["forced_prune"] += int(rows.size - by_rules.sum())
         u = np.where(commit_keep, ucb, -np.inf)
         ustar = u.max(axis=1)
         own = u.argmax(axis=1)          # the lowest index among exact maxima
@@ -305,20 +328,20 @@ class EveryInstanceChecker:
             near = commit_keep & ((ustar[:, None] - ucb) <= tol[:, None])
         valid = (ga >= 0) & (ga < K)
         gac = np.clip(ga, 0, K - 1)
-        ok = ~dec | (valid & near[np.arange(len(ga)), gac])
+        ok = ~dec | by_rules | (valid & near[np.arange(len(ga)), gac])
         if not ok.all():
             i = int(np.flatnonzero(~ok)[0])
             gu = ucb[i, ga[i]] if valid[i] else None
             self.fail(f"action mismatch at t={t}, instance {self.ids[i]}: GPU {ga[i]} (UCB {gu}), "
                       f"oracle {own[i]} (UCB {ustar[i]})")
         # exact ties (every near arm bit-identical to the best): lowest index on both sides
-        exact = dec & (near.sum(axis=1) > 1) & np.all(~near | (ucb == ustar[:, None]), axis=1)
+        exact = dec & ~by_rules & (near.sum(axis=1) > 1) & np.all(~near | (ucb == ustar[:, None]), axis=1)
         wrong = exact & (ga != own)
         if wrong.any():
             i = int(np.flatnonzero(wrong)[0])
             self.fail(f"exact tie broken wrongly at t={t}, instance {self.ids[i]}: {ga[i]} vs {own[i]}")
         st["exact_tie_steps"] += int(exact.sum())
-        st["forced"] += int((dec & (ga != own)).sum())
+        st["forced"] += int((dec & ~by_rules & (ga != own)).sum())
         st["decisions"] += int(dec.sum())
         return np.where(dec, ga, action).astype(np.int32), commit_keep
 
@@ -337,8 +360,9 @@ def compare_every_instance(wl, T, rec, ids):
     ids = np.asarray(ids)
     arrivals, noise = exogenous(wl, ids, T)
     chk = EveryInstanceChecker(wl.name, wl.K, ids, np.asarray(rec["a"]), np.asarray(rec["mask"]),
-                               np.asarray(rec["x"]), np.asarray(rec["r"]))
-    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk)
+                               np.asarray(rec["x"]), np.asarray(rec["r"]), rules=wl.prune,
+                               cascade_k=wl.cascade_k)
+    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14))
     st = chk.finish()
     st["oracle"] = out["oracle"]
     return st

@@ -4,8 +4,9 @@ score probes of the full-size parity tests: every instance of cfg2 (4,096)
 and cfg5 (1,024), every fourth of cfg3 and every sixteenth of cfg4 (4,096
 each, the last instance included), closed loop, at every step: contexts,
 rewards, prune decisions and actions (identical except at near-ties), then
-the final models.  (cfg1 is a single instance, compared in full by the
-parity tests.)
+the final models.  The same for their variants with the paper's pruning
+rules (cfg2p ... cfg5p).  (cfg1 is a single instance, compared in full by
+the parity tests.)
 
 With AGFT_EVERY_INSTANCE=1, every instance of cfg3 (16,384) and cfg4 (65,536)
 as well, in parts that share one GPU run per workload (minutes of oracle time
@@ -23,7 +24,8 @@ from paper_2508_01744_amd import run_closed_loop
 
 pytestmark = pytest.mark.gpu
 
-STRIDE = {"cfg2": 1, "cfg3": 4, "cfg4": 16, "cfg5": 1}
+STRIDE = {"cfg2": 1, "cfg3": 4, "cfg4": 16, "cfg5": 1,
+          "cfg2p": 1, "cfg3p": 4, "cfg4p": 16, "cfg5p": 1}
 
 
 @pytest.mark.parametrize("name", sorted(STRIDE))
@@ -39,7 +41,7 @@ def test_many_instances_full_size(name):
     st = parity.compare_every_instance(wl, wl.T, rec, ids)
     wth, wai = compare_model(out["tuner"], st["oracle"], ids, 1e-3, 1e-4)
     say(f"[every] {wl.name}: {st['decisions']} decisions, forced {st['forced']}, prune forced "
-        f"{st['forced_prune']}, exact-tie steps {st['exact_tie_steps']}, ctx err {st['max_ctx_err']:.2e}, "
+        f"{st['forced_prune']}, rules forced {st['forced_rules']}, exact-tie steps {st['exact_tie_steps']}, ctx err {st['max_ctx_err']:.2e}, "
         f"reward err {st['max_reward_err']:.2e}, theta err {wth:.2e}, Ainv err {wai:.2e}")
     del out
     torch.cuda.empty_cache()

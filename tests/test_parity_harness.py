@@ -186,3 +186,28 @@ def test_every_instance_planted_difference_fails(plant):
               "prune": "prune mismatch", "exact_tie": "exact tie"}[plant]
     with pytest.raises(parity.ParityError, match=expect):
         parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
+
+
+def test_every_instance_with_paper_rules_passes():
+    from agft_workloads import get_workload
+    wl = get_workload("cfg2p", B=6, T=200)
+    rec, out = _closed_record(wl)
+    assert wl.prune & 14 and not out["keep"][-1].all()
+    st = parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
+    assert st["decisions"] == wl.B * wl.T and st["forced"] == 0 and st["forced_rules"] == 0
+
+
+def test_every_instance_rule_removal_planted_fails():
+    """An arm that the paper's rules removed far from any threshold, kept in
+    the record's mask from then on."""
+    from agft_workloads import get_workload
+    wl = get_workload("cfg2p", B=6, T=200)
+    rec, out = _closed_record(wl)
+    keep = out["keep"]
+    gone = keep[:-1] & ~keep[1:]                 # removed at step t + 1
+    t, i, k = map(int, np.argwhere(gone)[0])
+    t += 1
+    words = rec["mask"].view(np.uint32)
+    words[t:, i, k // 32] |= np.uint32(1 << (k % 32))
+    with pytest.raises(parity.ParityError, match="prune mismatch"):
+        parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
