@@ -497,18 +497,18 @@ int occupancy_for(const agft_config &c, int tail) {
     return c.d == 16 && tail == 3 && !(c.prune_rule & 14) ? 6 : 7;
 }
 
-template <int D, int TF, int W>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(W)))
+template <int D, int TF, int W, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(W)))
 void agft_step_kernel(StepArgs p) {
     using R = Rec<D, TF>;
     constexpr int G = R::G, S = R::S;
     constexpr int NQ = (R::R + kWave - 1) / kWave;   // update-record chunks per thread (>= 64 threads)
     const int inst = blockIdx.x;
     const int tid = threadIdx.x;
-    const int nthr = blockDim.x;
+    constexpr int nthr = NW * kWave;   // the launch's workgroup width, fixed per instantiation
     const int lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-    const int nwave = nthr / kWave;
+    constexpr int nwave = NW;
     const int K = p.K;
     const int KW = p.KW;
     const int j = tid % G;           // slot of this lane within its arm's group
@@ -1298,6 +1298,16 @@ T *at(char *base, size_t off) {
     return reinterpret_cast<T *>(base + off);
 }
 
+// The step kernel for one or four wavefronts per workgroup (the two widths
+// waves_for chooses), each compiled for its width.
+template <int D, int TF, int W>
+void launch_step(int waves, unsigned grid, size_t lds, hipStream_t stream, const StepArgs &p) {
+    if (waves == 1)
+        hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 1>), dim3(grid), dim3(kWave), lds, stream, p);
+    else
+        hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 4>), dim3(grid), dim3(4 * kWave), lds, stream, p);
+}
+
 }  // namespace
 
 extern "C" {
@@ -1424,23 +1434,24 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     const int waves = shape.waves;
     p.early_update = shape.early_update;
     p.keep_stats = stats_kept(c) ? 1 : 0;
-    const dim3 grid((unsigned)c.B), block((unsigned)(kWave * waves));
+    if (waves != 1 && waves != 4) return AGFT_E_UNSUPPORTED;
+    const unsigned grid = (unsigned)c.B;
     const size_t lds = step_lds_bytes(c.K);
     const bool packed_tails = shape.tail_floats == 3;
+    hipStream_t s = h->stream;
     switch (c.d) {
         case 8:
-            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<8, 3, 7>), grid, block, lds, h->stream, p);
-            else hipLaunchKernelGGL((agft_step_kernel<8, 4, 7>), grid, block, lds, h->stream, p);
+            if (packed_tails) launch_step<8, 3, 7>(waves, grid, lds, s, p);
+            else launch_step<8, 4, 7>(waves, grid, lds, s, p);
             break;
         case 16:
-            if (packed_tails && shape.simd_waves == 6)
-                hipLaunchKernelGGL((agft_step_kernel<16, 3, 6>), grid, block, lds, h->stream, p);
-            else if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<16, 3, 7>), grid, block, lds, h->stream, p);
-            else hipLaunchKernelGGL((agft_step_kernel<16, 4, 7>), grid, block, lds, h->stream, p);
+            if (packed_tails && shape.simd_waves == 6) launch_step<16, 3, 6>(waves, grid, lds, s, p);
+            else if (packed_tails) launch_step<16, 3, 7>(waves, grid, lds, s, p);
+            else launch_step<16, 4, 7>(waves, grid, lds, s, p);
             break;
         case 32:
-            if (packed_tails) hipLaunchKernelGGL((agft_step_kernel<32, 3, 4>), grid, block, lds, h->stream, p);
-            else hipLaunchKernelGGL((agft_step_kernel<32, 4, 4>), grid, block, lds, h->stream, p);
+            if (packed_tails) launch_step<32, 3, 4>(waves, grid, lds, s, p);
+            else launch_step<32, 4, 4>(waves, grid, lds, s, p);
             break;
         default: return AGFT_E_UNSUPPORTED;
     }
