@@ -162,6 +162,8 @@ void ora_set_ph(void *h, int i, const float *stats, float margin, long last, lon
 void ora_set_refine(void *h, int on, int period, int stride, int half, int mature, int min_n);
 void ora_get_window(const void *h, int i, int *lo, int *hi, int *stride);
 void ora_set_window(void *h, int i, int lo, int hi, int stride);
+void ora_get_ph_all(const void *h, float *stats, float *margin, long *last, long *mode);
+void ora_get_window_all(const void *h, int *win);
 
 static int all_finite(const double *v, int n)
 {
@@ -312,6 +314,25 @@ void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, l
     if (margin) *margin = o->ph_margin[i];
     if (last) *last = o->ph_last[i];
     if (mode) *mode = o->mode[i];
+}
+
+/* Every instance's Page-Hinkley state at once: stats [B][6], margin [B],
+ * last alarm round [B], mode [B] (a copy; for the harness's batch checks). */
+void ora_get_ph_all(const void *h, float *stats, float *margin, long *last, long *mode)
+{
+    const ora_t *o = (const ora_t *)h;
+    const size_t B = (size_t)o->B;
+    memcpy(stats, o->ph, sizeof(float) * 6 * B);
+    memcpy(margin, o->ph_margin, sizeof(float) * B);
+    memcpy(last, o->ph_last, sizeof(long) * B);
+    memcpy(mode, o->mode, sizeof(long) * B);
+}
+
+/* Every instance's action space at once: win [B][3] = lo, hi, stride (a copy). */
+void ora_get_window_all(const void *h, int *win)
+{
+    const ora_t *o = (const ora_t *)h;
+    memcpy(win, o->win, sizeof(int) * 3 * (size_t)o->B);
 }
 
 /* Overwrite instance i's Page-Hinkley state and mode (the parity harness

@@ -38,6 +38,8 @@ def _declare(lib):
     lib.ora_set_ph.argtypes = [P, I, P, ctypes.c_float, L, L]
     lib.ora_set_refine.argtypes = [P, I, I, I, I, I, I]
     lib.ora_get_window.argtypes = [P, I, P, P, P]
+    lib.ora_get_ph_all.argtypes = [P, P, P, P, P]
+    lib.ora_get_window_all.argtypes = [P, P]
     lib.ora_set_window.argtypes = [P, I, I, I, I]
     lib.ora_commit.argtypes = [P, P, P, P]
     lib.ora_flush.argtypes = [P, P]
@@ -117,6 +119,22 @@ class Oracle:
         v = [ctypes.c_int(0) for _ in range(3)]
         self.lib.ora_get_window(self.h, int(i), *(ctypes.byref(q) for q in v))
         return tuple(q.value for q in v)
+
+    def page_hinkley_all(self):
+        """Every instance's (stats [B][6] float32, margin [B] float32, last alarm
+        round [B], mode [B])."""
+        stats = np.empty((self.B, 6), dtype=np.float32)
+        margin = np.empty(self.B, dtype=np.float32)
+        last = np.empty(self.B, dtype=np.int64)
+        mode = np.empty(self.B, dtype=np.int64)
+        self.lib.ora_get_ph_all(self.h, _ptr(stats), _ptr(margin), _ptr(last), _ptr(mode))
+        return stats, margin, last, mode
+
+    def windows(self):
+        """Every instance's action space, [B][3] = (lo, hi, stride)."""
+        win = np.empty((self.B, 3), dtype=np.int32)
+        self.lib.ora_get_window_all(self.h, _ptr(win))
+        return win
 
     def set_window(self, i, lo, hi, stride):
         self.lib.ora_set_window(self.h, int(i), int(lo), int(hi), int(stride))

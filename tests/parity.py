@@ -246,18 +246,97 @@ class EveryInstanceChecker:
     open, it adopts the GPU's).  With the paper's rules (bits 2, 4, 8) an
     arm may also be kept or removed differently when its rule comparison, or
     that of a higher arm whose cascade covers it, sat within TIE of the
-    threshold; the oracle then adopts the GPU's active set and action.  For
-    the workloads without the switch or the refinement.
+    threshold; the oracle then adopts the GPU's active set and action.  With
+    the switch, the test state after every step (within PH_TOL; an alarm one
+    side raised alone only where the oracle's margin was within PH_TIE, then
+    adopted with the GPU's decision); with the refinement, the action space
+    after every step (a different anchor only at a statistical refinement
+    whose candidates' mean rewards were within MEAN_TIE, then adopted): the
+    rules of Checker, on every instance at once.
 
     g_a [T][n] actions, g_words [T][n][KW] mask words after each step,
-    g_x [T][n][d] contexts and g_r [T][n] rewards (reward of decision t)."""
+    g_x [T][n][d] contexts, g_r [T][n] rewards (reward of decision t),
+    g_ph [T][n][9] test words and g_win [T][n][3] action spaces after each
+    step (with the switch and the refinement)."""
 
-    def __init__(self, name, K, ids, g_a, g_words, g_x, g_r, rules=0, cascade_k=0):
+    def __init__(self, name, K, ids, g_a, g_words, g_x, g_r, rules=0, cascade_k=0, g_ph=None,
+                 g_win=None, refine=None):
         self.name, self.K, self.ids = name, K, np.asarray(ids)
         self.g_a, self.g_words, self.g_x, self.g_r = g_a, g_words, g_x, g_r
         self.rules, self.cascade_k = rules, cascade_k
+        self.g_ph, self.g_win, self.refine = g_ph, g_win, refine
+        self.oracle = None
         self.st = dict(max_ctx_err=0.0, max_reward_err=0.0, forced=0, forced_prune=0, forced_rules=0,
-                       exact_tie_steps=0, decisions=0, no_decision=0, instances=len(self.ids))
+                       exact_tie_steps=0, decisions=0, no_decision=0, instances=len(self.ids),
+                       max_ph_err=0.0, forced_ph=0, forced_mode=0, greedy_decisions=0,
+                       refinements=0, forced_window=0)
+
+    def bind(self, oracle):
+        self.oracle = oracle
+
+    def _check_ph(self, t):
+        """Test state of every instance after step t; returns the rows whose
+        decision the two sides took in different modes (adopted as the GPU's)."""
+        g = np.asarray(self.g_ph[t], dtype=np.int32)
+        g_mode, g_last = g[:, 0].astype(np.int64), g[:, 7].astype(np.int64)
+        g_stats = np.ascontiguousarray(g[:, 1:7]).view(np.float32)
+        g_margin = np.ascontiguousarray(g[:, 8]).view(np.float32)
+        o_stats, o_margin, o_last, o_mode = self.oracle.page_hinkley_all()
+        same = (g_mode == o_mode) & (g_last == o_last)
+        if same.any():
+            a, b = g_stats[same].astype(np.float64), o_stats[same].astype(np.float64)
+            err = np.abs(a - b) / np.maximum(1.0, np.abs(b))
+            self.st["max_ph_err"] = max(self.st["max_ph_err"], float(err.max()))
+            if err.max() > PH_TOL:
+                i = int(np.flatnonzero(same)[np.argmax(err.max(axis=1))])
+                self.fail(f"Page-Hinkley statistics differ at t={t}, instance {self.ids[i]}: "
+                          f"{g_stats[i]} vs {o_stats[i]}")
+        mode_rows = np.zeros(len(g_mode), dtype=bool)
+        for i in np.flatnonzero(~same):
+            if g_last[i] == o_last[i] or abs(float(o_margin[i])) > PH_TIE:
+                self.fail(f"Page-Hinkley test differs at t={t}, instance {self.ids[i]}: GPU mode "
+                          f"{g_mode[i]}, last alarm {g_last[i]}; oracle mode {o_mode[i]}, last alarm "
+                          f"{o_last[i]}, margin {o_margin[i]}")
+            self.oracle.set_page_hinkley(int(i), g_stats[i], float(g_margin[i]), int(g_last[i]), int(g_mode[i]))
+            self.st["forced_ph"] += 1
+            if (g_mode[i] >= 0) != (o_mode[i] >= 0):
+                self.st["forced_mode"] += 1
+                mode_rows[i] = True
+        return mode_rows, g_mode
+
+    def after_commit(self, t):
+        """Action spaces of every instance once step t is committed."""
+        if self.g_win is None:
+            return
+        rf = self.refine
+        g = np.asarray(self.g_win[t], dtype=np.int64)
+        o = self.oracle.windows().astype(np.int64)
+        if t > 0 and t % rf["refine_period"] == 0:
+            self.st["refinements"] += int((g[:, 2] == 1).sum())
+        stat_step = t > 0 and t % rf["refine_period"] == 0 and t < rf["refine_mature"]
+        h = rf["refine_half"]
+
+        def anchor(lo, hi):
+            if lo > 0:
+                return lo + h
+            if hi < self.K - 1:
+                return hi - h
+            return None
+        for i in np.flatnonzero((g != o).any(axis=1)):
+            a_o, a_g = anchor(o[i, 0], o[i, 1]), anchor(g[i, 0], g[i, 1])
+            ok = stat_step and a_o is not None and a_g is not None and g[i, 2] == 1
+            if ok:
+                st = self.oracle.get(int(i))
+                n, rs = st["nsel"], st["rsum"]
+                ok = n[a_g] >= rf["refine_min_n"] and n[a_o] >= rf["refine_min_n"]
+                if ok:
+                    m_o, m_g = rs[a_o] / n[a_o], rs[a_g] / n[a_g]
+                    ok = abs(m_o - m_g) <= MEAN_TIE * max(1.0, abs(m_o))
+            if not ok:
+                self.fail(f"action space differs after t={t}, instance {self.ids[i]}: GPU "
+                          f"{tuple(g[i])}, oracle {tuple(o[i])}")
+            self.oracle.set_window(int(i), int(g[i, 0]), int(g[i, 1]), int(g[i, 2]))
+            self.st["forced_window"] += 1
 
     def _rules_ambiguous(self, margins):
         """[n][K]: arm k's removal by rules 2/4/8 could go either way."""
@@ -290,6 +369,10 @@ class EveryInstanceChecker:
                 self.fail(f"reward mismatch at t={t - 1}, instance {self.ids[i]}: {gr[i]} vs {r_prev[i]}")
         ga = np.asarray(self.g_a[t], dtype=np.int64)
         dec = action >= 0
+        mode_rows = np.zeros(len(ga), dtype=bool)
+        if self.g_ph is not None:
+            mode_rows, g_mode = self._check_ph(t)
+            self.st["greedy_decisions"] += int(((g_mode >= 0) & dec & ~mode_rows).sum())
         st["no_decision"] += int((~dec).sum())
         if np.any(~dec & (ga != -1)):
             i = int(np.flatnonzero(~dec & (ga != -1))[0])
@@ -297,7 +380,7 @@ class EveryInstanceChecker:
         act = np.isfinite(ucb)
         g_keep = mask_words_to_bool(self.g_words[t], K)
         commit_keep = keep.copy()
-        diff = (g_keep != keep) & dec[:, None]
+        diff = (g_keep != keep) & (dec & ~mode_rows)[:, None]
         rows = np.flatnonzero(diff.any(axis=1))
         by_rules = np.zeros(len(ga), dtype=bool)
         if rows.size:
@@ -328,20 +411,22 @@ class EveryInstanceChecker:
             near = commit_keep & ((ustar[:, None] - ucb) <= tol[:, None])
         valid = (ga >= 0) & (ga < K)
         gac = np.clip(ga, 0, K - 1)
-        ok = ~dec | by_rules | (valid & near[np.arange(len(ga)), gac])
+        skip = by_rules | mode_rows
+        commit_keep[mode_rows] = g_keep[mode_rows]
+        ok = ~dec | skip | (valid & near[np.arange(len(ga)), gac])
         if not ok.all():
             i = int(np.flatnonzero(~ok)[0])
             gu = ucb[i, ga[i]] if valid[i] else None
             self.fail(f"action mismatch at t={t}, instance {self.ids[i]}: GPU {ga[i]} (UCB {gu}), "
                       f"oracle {own[i]} (UCB {ustar[i]})")
         # exact ties (every near arm bit-identical to the best): lowest index on both sides
-        exact = dec & ~by_rules & (near.sum(axis=1) > 1) & np.all(~near | (ucb == ustar[:, None]), axis=1)
+        exact = dec & ~skip & (near.sum(axis=1) > 1) & np.all(~near | (ucb == ustar[:, None]), axis=1)
         wrong = exact & (ga != own)
         if wrong.any():
             i = int(np.flatnonzero(wrong)[0])
             self.fail(f"exact tie broken wrongly at t={t}, instance {self.ids[i]}: {ga[i]} vs {own[i]}")
         st["exact_tie_steps"] += int(exact.sum())
-        st["forced"] += int((dec & ~by_rules & (ga != own)).sum())
+        st["forced"] += int((dec & ~skip & (ga != own)).sum())
         st["decisions"] += int(dec.sum())
         return np.where(dec, ga, action).astype(np.int32), commit_keep
 
@@ -355,14 +440,19 @@ def compare_every_instance(wl, T, rec, ids):
     batch, in order) through the oracle and its environment and compare each
     one's contexts, rewards, prune decisions and actions at every step; raise
     ParityError on a violation.  rec: host arrays recorded for those
-    instances, a [T][n], mask [T][n][KW], x [T][n][d], r [T][n] (the probe
+    instances, a [T][n], mask [T][n][KW], x [T][n][d], r [T][n], and ph
+    [T][n][9] with the switch, win [T][n][3] with the refinement (the probe
     records of paper_2508_01744_amd.run_closed_loop)."""
     ids = np.asarray(ids)
     arrivals, noise = exogenous(wl, ids, T)
     chk = EveryInstanceChecker(wl.name, wl.K, ids, np.asarray(rec["a"]), np.asarray(rec["mask"]),
                                np.asarray(rec["x"]), np.asarray(rec["r"]), rules=wl.prune,
-                               cascade_k=wl.cascade_k)
-    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14))
+                               cascade_k=wl.cascade_k,
+                               g_ph=np.asarray(rec["ph"]) if wl.exploit else None,
+                               g_win=np.asarray(rec["win"]) if wl.refine else None,
+                               refine=wl.refinement() if wl.refine else None)
+    out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14),
+                          on_create=chk.bind, on_commit=chk.after_commit)
     st = chk.finish()
     st["oracle"] = out["oracle"]
     return st

@@ -8,9 +8,12 @@ the final models.  The same for their variants with the paper's pruning
 rules (cfg2p ... cfg5p).  (cfg1 is a single instance, compared in full by
 the parity tests.)
 
-With AGFT_EVERY_INSTANCE=1, every instance of cfg3 (16,384) and cfg4 (65,536)
-as well, in parts that share one GPU run per workload (minutes of oracle time
-on the host, so not part of the default run)."""
+With AGFT_EVERY_INSTANCE=1 (minutes of oracle time on the host, so not part
+of the default run), the same for the variants with the switch to
+exploitation (cfg2e ... cfg5e, with the test state after every step), the
+refinement (cfg2r ... cfg5r, with the action space after every step),
+cfg4pe and cfg4per; and every instance of cfg3 (16,384) and cfg4 (65,536),
+in parts that share one GPU run per workload."""
 import os
 
 import numpy as np
@@ -24,12 +27,17 @@ from paper_2508_01744_amd import run_closed_loop
 
 pytestmark = pytest.mark.gpu
 
-STRIDE = {"cfg2": 1, "cfg3": 4, "cfg4": 16, "cfg5": 1,
-          "cfg2p": 1, "cfg3p": 4, "cfg4p": 16, "cfg5p": 1}
+STRIDE = {f"cfg{n}{v}": {2: 1, 3: 4, 4: 16, 5: 1}[n] for n in (2, 3, 4, 5) for v in ("", "p", "e", "r")}
+STRIDE.update(cfg4pe=16, cfg4per=16)
+EVERY = os.environ.get("AGFT_EVERY_INSTANCE") == "1"
+OPT_IN = "set AGFT_EVERY_INSTANCE=1 (minutes of oracle time)"
+FIELDS = ("a", "mask", "x", "r", "ph", "win")
 
 
 @pytest.mark.parametrize("name", sorted(STRIDE))
 def test_many_instances_full_size(name):
+    if name[4:] not in ("", "p") and not EVERY:
+        pytest.skip(OPT_IN)
     wl = get_workload(name)
     ids = list(range(0, wl.B, STRIDE[name]))
     if ids[-1] != wl.B - 1:
@@ -37,11 +45,12 @@ def test_many_instances_full_size(name):
     say(f"[every] {wl.name} B={wl.B} K={wl.K} d={wl.d} T={wl.T}: {len(ids)} instances compared")
     arr, noi = exogenous(wl)
     out = run_closed_loop(wl, ENV, arr, noi, probes=ids)
-    rec = {k: out["probes"][k].numpy() for k in ("a", "mask", "x", "r")}
+    rec = {k: out["probes"][k].numpy() for k in FIELDS}
     st = parity.compare_every_instance(wl, wl.T, rec, ids)
     wth, wai = compare_model(out["tuner"], st["oracle"], ids, 1e-3, 1e-4)
     say(f"[every] {wl.name}: {st['decisions']} decisions, forced {st['forced']}, prune forced "
-        f"{st['forced_prune']}, rules forced {st['forced_rules']}, exact-tie steps {st['exact_tie_steps']}, ctx err {st['max_ctx_err']:.2e}, "
+        f"{st['forced_prune']}, rules forced {st['forced_rules']}, test forced {st['forced_ph']}, greedy "
+        f"{st['greedy_decisions']}, refinements {st['refinements']}, windows forced {st['forced_window']}, exact-tie steps {st['exact_tie_steps']}, ctx err {st['max_ctx_err']:.2e}, "
         f"reward err {st['max_reward_err']:.2e}, theta err {wth:.2e}, Ainv err {wai:.2e}")
     del out
     torch.cuda.empty_cache()
@@ -59,14 +68,12 @@ def _gpu_run(name):
         wl = get_workload(name)
         arr, noi = exogenous(wl)
         out = run_closed_loop(wl, ENV, arr, noi, probes=range(wl.B))
-        rec = {k: out["probes"][k].numpy() for k in ("a", "mask", "x", "r")}
+        rec = {k: out["probes"][k].numpy() for k in FIELDS}
         _runs[name] = (wl, rec, out["tuner"])
     return _runs[name]
 
 
-@pytest.mark.skipif(os.environ.get("AGFT_EVERY_INSTANCE") != "1",
-                    reason="every instance of cfg3 and cfg4 takes minutes of oracle time; "
-                           "set AGFT_EVERY_INSTANCE=1")
+@pytest.mark.skipif(not EVERY, reason=OPT_IN)
 @pytest.mark.parametrize("name,part", [(w, q) for w in sorted(PARTS) for q in range(PARTS[w])])
 def test_every_instance_full_size(name, part):
     wl, rec, tuner = _gpu_run(name)

@@ -211,3 +211,72 @@ def test_every_instance_rule_removal_planted_fails():
     words[t:, i, k // 32] |= np.uint32(1 << (k % 32))
     with pytest.raises(parity.ParityError, match="prune mismatch"):
         parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
+
+
+def _closed_record_full(wl):
+    """As _closed_record, with the test words and action spaces after each step."""
+    from agft_workloads import exogenous
+    from oracle import run_closed_loop
+    arrivals, noise = exogenous(wl, None, wl.T)
+    T, B = wl.T, wl.B
+    ph = np.empty((T, B, 9), np.int32)
+    win = np.empty((T, B, 3), np.int32)
+    box = {}
+
+    def commit(t):
+        o = box["ora"]
+        if wl.exploit:
+            stats, margin, last, mode = o.page_hinkley_all()
+            ph[t, :, 0] = mode
+            ph[t, :, 1:7] = stats.view(np.int32)
+            ph[t, :, 7] = last
+            ph[t, :, 8] = margin.view(np.int32)
+        win[t] = o.windows()
+    out = run_closed_loop(wl, arrivals, noise, T=T, record=True,
+                          on_create=lambda o: box.__setitem__("ora", o), on_commit=commit)
+    K = wl.K
+    words = np.zeros((T, B, (K + 31) // 32), np.int64)
+    for k in range(K):
+        words[:, :, k // 32] |= out["keep"][:, :, k].astype(np.int64) << (k % 32)
+    rec = dict(a=out["actions"].copy(), mask=words.astype(np.uint32).view(np.int32),
+               x=out["x"].astype(np.float32), r=out["r"].astype(np.float32), ph=ph, win=win)
+    return rec, out
+
+
+def test_every_instance_switch_and_refinement_pass():
+    from agft_workloads import get_workload
+    wl = get_workload("cfg2e", B=6, T=300)
+    rec, _ = _closed_record_full(wl)
+    assert (rec["ph"][-1, :, 0] >= 0).any()
+    st = parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
+    assert st["greedy_decisions"] > 0 and st["forced_ph"] == 0 and st["forced"] == 0
+    wl = get_workload("cfg2r", B=6, T=220)
+    rec, _ = _closed_record_full(wl)
+    st = parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
+    assert st["refinements"] > 0 and st["forced_window"] == 0 and st["forced"] == 0
+
+
+@pytest.mark.parametrize("plant", ["switch_late", "statistic", "window"])
+def test_every_instance_switch_or_window_planted_fails(plant):
+    from agft_workloads import get_workload
+    if plant == "window":
+        wl = get_workload("cfg2r", B=6, T=220)
+        rec, _ = _closed_record_full(wl)
+        t = 150                                  # after a refinement: a window one arm off
+        rec["win"][t:, 2, :2] += 1
+        expect = "action space differs"
+    else:
+        wl = get_workload("cfg2e", B=6, T=300)
+        rec, _ = _closed_record_full(wl)
+        modes = rec["ph"][-1, :, 0]
+        i = int(np.flatnonzero(modes >= 0)[0])
+        t_sw = int(modes[i])
+        if plant == "switch_late":
+            rec["ph"][t_sw, i, 0] = -1
+            expect = "Page-Hinkley test differs"
+        else:                                    # the running mean off by 1e-3
+            st = rec["ph"][t_sw // 2, i, 1:7].view(np.float32)
+            st[1] += np.float32(1e-3)
+            expect = "Page-Hinkley statistics differ"
+    with pytest.raises(parity.ParityError, match=expect):
+        parity.compare_every_instance(wl, wl.T, rec, range(wl.B))
