@@ -45,15 +45,17 @@
  * There is no rank-1 identity here: that is the GPU path's business.
  *
  * Exploitation (Sec. 4.2, Eq. 2), when enabled: each reward folded in also
- * feeds a two-sided Page-Hinkley test on the instance's reward sequence
- * (running mean rbar_n; m+ += r - rbar_n - delta, m- += rbar_n - r - delta;
- * an alarm when m+ - min m+ or m- - min m- exceeds lambda, after which the
- * test restarts).  The sequence counts as stable once t >= min_rounds and no
- * alarm was raised in the last `window` rounds; from then on the instance
- * exploits for good: a_t = argmax over the active arms of theta_k^T x_t
- * (reported as both UCB and LCB), rule 1 is not applied, updates go on.
- * The test decides an integer (the switch round), so it runs in single
- * precision with the GPU kernel's operation order; the model stays double.
+ * feeds a two-sided Page-Hinkley test on the instance's reward sequence, in
+ * double precision like everything else here.  With r_1..r_n the rewards
+ * since the test last (re)started and rbar_s the mean of r_1..r_s:
+ *   m+_n = sum_{s<=n} (r_s - rbar_s - delta),  M+_n = min(0, m+_1, ..., m+_n),
+ *   m-_n = sum_{s<=n} (rbar_s - r_s - delta),  M-_n = min(0, m-_1, ..., m-_n);
+ * an alarm is raised when m+_n - M+_n or m-_n - M-_n exceeds lambda, and the
+ * test restarts (n = 0).  The sequence counts as stable once t >= min_rounds
+ * and no alarm was raised in the last `window` rounds; from then on the
+ * instance exploits for good: a_t = argmax over the active arms of
+ * theta_k^T x_t (reported as both UCB and LCB), rule 1 is not applied,
+ * updates go on.
  *
  * Mixed-maturity refinement (Sec. 4.4), when enabled: the action space is a
  * set of arms on the K-arm grid (one arm step plays the paper's 15 MHz),
@@ -90,20 +92,30 @@
 
 #define ORA_MAXD 64
 
+/* State of one two-sided Page-Hinkley test (see the header). */
+struct ph_test {
+    double n;       /* rewards since the last restart */
+    double sum;     /* their sum: rbar_n = sum / n */
+    double up;      /* m+_n */
+    double up_min;  /* M+_n (0 at a restart) */
+    double dn;      /* m-_n */
+    double dn_min;  /* M-_n */
+};
+
 typedef struct {
     int B, K, d, prune, period, sched;
     double lambda, alpha0;
     /* parameters of rules 2-8 */
     int ext_rounds, ext_min_n, hist_after, hist_min_n, hist_min_arms, cascade_k;
     double ext_thr, hist_kappa;
-    /* exploitation switch (Page-Hinkley, single precision) */
+    /* exploitation switch (Page-Hinkley test on the rewards) */
     int exploit, ph_window, ph_min_rounds;
-    float ph_delta, ph_lambda;
-    float *ph;              /* [B][6]        n, mean, m+, min m+, m-, min m- */
+    double ph_delta, ph_lambda;
+    struct ph_test *ph;     /* [B]           one test per instance */
     /* mixed-maturity refinement */
     int refine, refine_period, refine_stride, refine_half, refine_mature, refine_min_n;
     int *win;               /* [B][3]        action space lo, hi, stride */
-    float *ph_margin;       /* [B]           lambda - larger statistic at the last test */
+    double *ph_margin;      /* [B]           lambda - larger statistic at the last test */
     long *ph_last;          /* [B]           round of the last alarm (0 at start) */
     long *mode;             /* [B]           -1 exploring, else the round exploitation began */
     double *A;              /* [B][K][d][d]  Eq. 3 */
@@ -157,12 +169,12 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
                    unsigned char *keep, int *action, double *margins);
 void ora_get_rsum(const void *h, int i, double *rsum);
 void ora_set_exploit(void *h, int on, double delta, double lambda, int window, int min_rounds);
-void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, long *mode);
-void ora_set_ph(void *h, int i, const float *stats, float margin, long last, long mode);
+void ora_get_ph(const void *h, int i, double *stats, double *margin, long *last, long *mode);
+void ora_set_ph(void *h, int i, const double *stats, double margin, long last, long mode);
 void ora_set_refine(void *h, int on, int period, int stride, int half, int mature, int min_n);
 void ora_get_window(const void *h, int i, int *lo, int *hi, int *stride);
 void ora_set_window(void *h, int i, int lo, int hi, int stride);
-void ora_get_ph_all(const void *h, float *stats, float *margin, long *last, long *mode);
+void ora_get_ph_all(const void *h, double *stats, double *margin, long *last, long *mode);
 void ora_get_window_all(const void *h, int *win);
 
 static int all_finite(const double *v, int n)
@@ -192,8 +204,8 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
     o->xprev = (double *)calloc((size_t)B * d, sizeof(double));
     o->aprev = (int *)malloc((size_t)B * sizeof(int));
     o->bad = (int *)calloc((size_t)B, sizeof(int));
-    o->ph = (float *)calloc((size_t)B * 6, sizeof(float));
-    o->ph_margin = (float *)malloc((size_t)B * sizeof(float));
+    o->ph = (struct ph_test *)calloc((size_t)B, sizeof(struct ph_test));
+    o->ph_margin = (double *)malloc((size_t)B * sizeof(double));
     o->ph_last = (long *)calloc((size_t)B, sizeof(long));
     o->mode = (long *)malloc((size_t)B * sizeof(long));
     o->win = (int *)malloc((size_t)B * 3 * sizeof(int));
@@ -280,37 +292,48 @@ void ora_set_exploit(void *h, int on, double delta, double lambda, int window, i
 {
     ora_t *o = (ora_t *)h;
     o->exploit = on;
-    o->ph_delta = (float)delta;
-    o->ph_lambda = (float)lambda;
+    o->ph_delta = delta;
+    o->ph_lambda = lambda;
     o->ph_window = window;
     o->ph_min_rounds = min_rounds;
 }
 
-/* One reward into instance i's Page-Hinkley test at round t (single precision). */
-static void page_hinkley(ora_t *o, int i, long t, double reward)
+/* One reward into instance i's Page-Hinkley test at round t. */
+static void page_hinkley(ora_t *o, int i, long t, double r)
 {
-    float *s = o->ph + (size_t)i * 6;
-    const float r = (float)reward;
-    s[0] = s[0] + 1.0f;
-    s[1] = s[1] + (r - s[1]) / s[0];
-    s[2] = s[2] + (r - s[1] - o->ph_delta);
-    s[3] = fminf(s[3], s[2]);
-    s[4] = s[4] + (s[1] - r - o->ph_delta);
-    s[5] = fminf(s[5], s[4]);
-    const float up = s[2] - s[3], down = s[4] - s[5];
-    o->ph_margin[i] = o->ph_lambda - (up > down ? up : down);
-    if (up > o->ph_lambda || down > o->ph_lambda) {
+    struct ph_test *p = o->ph + i;
+    p->n += 1.0;
+    p->sum += r;
+    const double rbar = p->sum / p->n;
+    p->up += (r - rbar) - o->ph_delta;
+    p->dn += (rbar - r) - o->ph_delta;
+    if (p->up < p->up_min) p->up_min = p->up;
+    if (p->dn < p->dn_min) p->dn_min = p->dn;
+    const double stat = fmax(p->up - p->up_min, p->dn - p->dn_min);
+    o->ph_margin[i] = o->ph_lambda - stat;
+    if (stat > o->ph_lambda) {
         o->ph_last[i] = t;
-        for (int q = 0; q < 6; ++q) s[q] = 0.0f;
+        memset(p, 0, sizeof(*p));
     }
+}
+
+/* The test state as six numbers: n, rbar_n (0 when n = 0), m+, M+, m-, M-. */
+static void ph_export(const struct ph_test *p, double *out)
+{
+    out[0] = p->n;
+    out[1] = p->n > 0.0 ? p->sum / p->n : 0.0;
+    out[2] = p->up;
+    out[3] = p->up_min;
+    out[4] = p->dn;
+    out[5] = p->dn_min;
 }
 
 /* Page-Hinkley state of instance i: stats[6] (n, mean, m+, min m+, m-, min m-),
  * the last margin, the last alarm round and the mode; outputs may be NULL. */
-void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, long *mode)
+void ora_get_ph(const void *h, int i, double *stats, double *margin, long *last, long *mode)
 {
     const ora_t *o = (const ora_t *)h;
-    if (stats) memcpy(stats, o->ph + (size_t)i * 6, sizeof(float) * 6);
+    if (stats) ph_export(o->ph + i, stats);
     if (margin) *margin = o->ph_margin[i];
     if (last) *last = o->ph_last[i];
     if (mode) *mode = o->mode[i];
@@ -318,12 +341,12 @@ void ora_get_ph(const void *h, int i, float *stats, float *margin, long *last, l
 
 /* Every instance's Page-Hinkley state at once: stats [B][6], margin [B],
  * last alarm round [B], mode [B] (a copy; for the harness's batch checks). */
-void ora_get_ph_all(const void *h, float *stats, float *margin, long *last, long *mode)
+void ora_get_ph_all(const void *h, double *stats, double *margin, long *last, long *mode)
 {
     const ora_t *o = (const ora_t *)h;
     const size_t B = (size_t)o->B;
-    memcpy(stats, o->ph, sizeof(float) * 6 * B);
-    memcpy(margin, o->ph_margin, sizeof(float) * B);
+    for (size_t i = 0; i < B; ++i) ph_export(o->ph + i, stats + 6 * i);
+    memcpy(margin, o->ph_margin, sizeof(double) * B);
     memcpy(last, o->ph_last, sizeof(long) * B);
     memcpy(mode, o->mode, sizeof(long) * B);
 }
@@ -335,12 +358,19 @@ void ora_get_window_all(const void *h, int *win)
     memcpy(win, o->win, sizeof(int) * 3 * (size_t)o->B);
 }
 
-/* Overwrite instance i's Page-Hinkley state and mode (the parity harness
- * adopts the GPU's when an alarm comparison sat within rounding of lambda). */
-void ora_set_ph(void *h, int i, const float *stats, float margin, long last, long mode)
+/* Overwrite instance i's Page-Hinkley state and mode from six numbers in the
+ * layout of ora_get_ph (the parity harness adopts the GPU's when an alarm
+ * comparison sat within rounding of lambda). */
+void ora_set_ph(void *h, int i, const double *stats, double margin, long last, long mode)
 {
     ora_t *o = (ora_t *)h;
-    memcpy(o->ph + (size_t)i * 6, stats, sizeof(float) * 6);
+    struct ph_test *p = o->ph + i;
+    p->n = stats[0];
+    p->sum = stats[1] * stats[0];
+    p->up = stats[2];
+    p->up_min = stats[3];
+    p->dn = stats[4];
+    p->dn_min = stats[5];
     o->ph_margin[i] = margin;
     o->ph_last[i] = last;
     o->mode[i] = mode;

@@ -35,7 +35,7 @@ def _declare(lib):
     lib.ora_get_rsum.argtypes = [P, I, P]
     lib.ora_set_exploit.argtypes = [P, I, D, D, I, I]
     lib.ora_get_ph.argtypes = [P, I, P, P, P, P]
-    lib.ora_set_ph.argtypes = [P, I, P, ctypes.c_float, L, L]
+    lib.ora_set_ph.argtypes = [P, I, P, D, L, L]
     lib.ora_set_refine.argtypes = [P, I, I, I, I, I, I]
     lib.ora_get_window.argtypes = [P, I, P, P, P]
     lib.ora_get_ph_all.argtypes = [P, P, P, P, P]
@@ -99,9 +99,10 @@ class Oracle:
                                  int(ph_window), int(ph_min_rounds))
 
     def page_hinkley(self, i):
-        """(stats[6] float32, last margin, last alarm round, mode) of instance i."""
-        stats = np.empty(6, dtype=np.float32)
-        margin = ctypes.c_float(0.0)
+        """(stats[6]: n, mean, m+, min m+, m-, min m-; last margin; last alarm
+        round; mode) of instance i, in double precision."""
+        stats = np.empty(6, dtype=np.float64)
+        margin = ctypes.c_double(0.0)
         last = ctypes.c_long(0)
         mode = ctypes.c_long(0)
         self.lib.ora_get_ph(self.h, int(i), _ptr(stats), ctypes.byref(margin), ctypes.byref(last),
@@ -121,10 +122,10 @@ class Oracle:
         return tuple(q.value for q in v)
 
     def page_hinkley_all(self):
-        """Every instance's (stats [B][6] float32, margin [B] float32, last alarm
-        round [B], mode [B])."""
-        stats = np.empty((self.B, 6), dtype=np.float32)
-        margin = np.empty(self.B, dtype=np.float32)
+        """Every instance's (stats [B][6], margin [B], last alarm round [B],
+        mode [B]), in double precision."""
+        stats = np.empty((self.B, 6), dtype=np.float64)
+        margin = np.empty(self.B, dtype=np.float64)
         last = np.empty(self.B, dtype=np.int64)
         mode = np.empty(self.B, dtype=np.int64)
         self.lib.ora_get_ph_all(self.h, _ptr(stats), _ptr(margin), _ptr(last), _ptr(mode))
@@ -141,7 +142,7 @@ class Oracle:
 
     def set_page_hinkley(self, i, stats, margin, last, mode):
         """Overwrite instance i's Page-Hinkley state and mode."""
-        st = np.ascontiguousarray(stats, dtype=np.float32)
+        st = np.ascontiguousarray(stats, dtype=np.float64)
         self.lib.ora_set_ph(self.h, int(i), _ptr(st), float(margin), int(last), int(mode))
 
     def set_heuristics(self, ext_rounds, ext_min_n, ext_thr, hist_after, hist_min_n, hist_kappa,

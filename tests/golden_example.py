@@ -36,3 +36,25 @@ def load_worked_example(path=os.path.join(GOLDEN, "linucb_worked_example.txt")):
     ex["final_Ainv"] = [ex["final_Ainv"][k] for k in range(K)]
     ex["final_theta"] = [ex["final_theta"][k] for k in range(K)]
     return ex
+
+
+def load_page_hinkley_example(path=os.path.join(GOLDEN, "page_hinkley_worked_example.txt")):
+    """The hand-worked Page-Hinkley example: parameters (delta, lambda, window,
+    min_rounds) and, per round, the reward entering it, the state after it
+    (n, mean, up, up_min, dn, dn_min), the margin, the alarm flag and the mode."""
+    ex = dict(rounds=[])
+    with open(path) as fh:
+        for line in fh:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            if line.startswith("round "):
+                f = dict(p.split("=") for p in line[6:].split())
+                ex["rounds"].append(dict(
+                    t=int(f["t"]), r=Fraction(f["r"]), alarm=int(f["alarm"]), mode=int(f["mode"]),
+                    state=[Fraction(f[k]) for k in ("n", "mean", "up", "up_min", "dn", "dn_min")],
+                    margin=Fraction(f["margin"])))
+            else:
+                key, val = [p.strip() for p in line.split("=")]
+                ex[key] = Fraction(val) if key in ("delta", "lambda") else int(val)
+    return ex

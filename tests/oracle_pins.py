@@ -446,22 +446,23 @@ ALL_PINS += [pin_extreme_pruning, pin_historical_pruning, pin_cascade_pruning,
 PH = dict(ph_delta=0.05, ph_lambda=5.0, ph_window=100, ph_min_rounds=100)
 
 
-def _ph_reference(rewards, delta, lam):
-    """Independent restatement of the two-sided Page-Hinkley test in float32:
-    returns the alarm rounds (reward s is folded in at round s + 1)."""
-    f = np.float32
-    alarms = []
-    n = f(0); mean = f(0); up = f(0); up_min = f(0); dn = f(0); dn_min = f(0)
-    for s, r in enumerate(np.asarray(rewards, dtype=np.float32)):
-        n = f(n + f(1))
-        mean = f(mean + f(f(r - mean) / n))
-        up = f(up + f(f(r - mean) - f(delta)))
-        up_min = min(up_min, up)
-        dn = f(dn + f(f(mean - r) - f(delta)))
-        dn_min = min(dn_min, dn)
-        if f(up - up_min) > f(lam) or f(dn - dn_min) > f(lam):
+def _ph_by_definition(rewards, delta, lam):
+    """Alarm rounds of the two-sided Page-Hinkley test computed from its
+    definition: after each restart, the cumulative sums are rebuilt from the
+    rewards seen since then, each running mean recomputed from scratch
+    (reward s enters at round s + 1)."""
+    alarms, seg = [], []
+    for s, r in enumerate(rewards):
+        seg.append(float(r))
+        up = dn = up_min = dn_min = 0.0
+        for q in range(len(seg)):
+            rbar = sum(seg[:q + 1]) / (q + 1)
+            up += seg[q] - rbar - delta
+            dn += rbar - seg[q] - delta
+            up_min, dn_min = min(up_min, up), min(dn_min, dn)
+        if max(up - up_min, dn - dn_min) > lam:
             alarms.append(s + 1)
-            n = mean = up = up_min = dn = dn_min = f(0)
+            seg = []
     return alarms
 
 
@@ -481,30 +482,78 @@ def _run_rewards(lib, rewards, K=3, d=2, ph=PH, rule=0, x_fn=None):
     return hist, ora
 
 
+def pin_page_hinkley_worked_example(lib):
+    """The hand-worked example under tests/golden/ (exact rationals): the
+    test's state, margin, alarm rounds and switch round after every round,
+    an upward and a downward alarm with a restart after each, and no test
+    once exploiting."""
+    from golden_example import load_page_hinkley_example
+    ex = load_page_hinkley_example()
+    ora = Oracle(1, 2, 2, 1.0, 1.0, 0, 0, 50, lib=lib)
+    ora.set_exploit(True, ph_delta=float(ex["delta"]), ph_lambda=float(ex["lambda"]),
+                    ph_window=ex["window"], ph_min_rounds=ex["min_rounds"])
+    x = np.array([[1.0, 0.5]])
+    rewards = {rd["t"] - 1: float(rd["r"]) for rd in ex["rounds"]}
+    ora.step(x, None)
+    last = 0
+    for rd in ex["rounds"]:
+        t = rd["t"]
+        ora.step(x, np.array([rewards[t - 1]]))
+        stats, margin, got_last, mode = ora.page_hinkley(0)
+        want = np.array([float(v) for v in rd["state"]])
+        assert np.allclose(stats, want, rtol=0, atol=1e-12), (t, stats, want)
+        assert abs(margin - float(rd["margin"])) <= 1e-12, (t, margin)
+        if rd["alarm"]:
+            last = t
+        assert got_last == last and mode == rd["mode"], (t, got_last, mode)
+
+
+def pin_page_hinkley_threshold_is_strict(lib):
+    """The test alarms when its statistic exceeds lambda, not when it reaches
+    it: with delta = 0 and lambda = 1, rewards 0, 2 bring m+ to exactly 1
+    (binary-exact) with no alarm; a further 2 brings it to 5/3 and alarms."""
+    hist, ora = _run_rewards(lib, [0.0, 2.0, 2.0, 2.0],
+                             ph=dict(ph_delta=0.0, ph_lambda=1.0, ph_window=50, ph_min_rounds=50))
+    # _run_rewards feeds reward s at round s + 1 and stops after the last
+    # decision, so the last reward is never fed: rounds 1..3 have run
+    stats, margin, last, mode = ora.page_hinkley(0)
+    assert last == 3 and np.all(stats == 0.0), (last, stats)
+    hist, ora = _run_rewards(lib, [0.0, 2.0, 0.0],
+                             ph=dict(ph_delta=0.0, ph_lambda=1.0, ph_window=50, ph_min_rounds=50))
+    stats, margin, last, mode = ora.page_hinkley(0)
+    assert last == 0 and margin == 0.0 and stats[2] == 1.0 and stats[3] == 0.0, (last, margin, stats)
+
+
 def pin_page_hinkley_switch_round(lib):
     """A stationary reward sequence never alarms, so exploitation starts at
-    round max(min_rounds, window); a step in the mean alarms at the round an
-    independent float32 restatement says, and postpones the switch to that
-    round plus the window."""
+    round max(min_rounds, window); a step of height h after s0 constant
+    rewards raises the upward statistic by h*s0/(s0+q) - delta at the q-th
+    round after it (the running mean moves by h/(s0+q) per round), so the
+    alarm comes at the first k whose partial sum exceeds lambda, and the
+    switch is postponed to that round plus the window; on noise, the alarm
+    rounds are those of the test's definition recomputed from scratch."""
     flat = [-1.0] * 160
     hist, ora = _run_rewards(lib, flat)
     assert ora.page_hinkley(0)[3] == 100
     assert all(h[1][h[3]] != h[2][h[3]] for h in hist[:100])       # UCB > LCB while exploring
     hist, ora = _run_rewards(lib, flat, ph=dict(PH, ph_min_rounds=130))
     assert ora.page_hinkley(0)[3] == 130
-    step = [-1.0] * 80 + [-0.2] * 200
-    alarms = _ph_reference(step, 0.05, 5.0)
-    assert alarms and 80 < alarms[0] < 120
+    s0, h, delta, lam = 80, 0.8, PH["ph_delta"], PH["ph_lambda"]
+    acc, k = 0.0, 0
+    while acc <= lam:
+        k += 1
+        acc += h * s0 / (s0 + k) - delta
+    step = [-1.0] * s0 + [-1.0 + h] * 200
     hist, ora = _run_rewards(lib, step)
     _, _, last, mode = ora.page_hinkley(0)
-    expect_last = max(a for a in alarms if a < mode) if mode >= 0 else alarms[-1]
-    assert last == expect_last and mode == max(100, last + 100)
+    assert last == s0 + k and mode == last + PH["ph_window"], (last, mode, s0 + k)
     noisy = list(np.random.default_rng(4).normal(-1.0, 0.4, 400))
     hist, ora = _run_rewards(lib, noisy)
-    alarms = _ph_reference(noisy, 0.05, 5.0)
+    alarms = _ph_by_definition(noisy, PH["ph_delta"], PH["ph_lambda"])
     _, _, last, mode = ora.page_hinkley(0)
-    before = [a for a in alarms if mode < 0 or a < mode]
-    assert last == (before[-1] if before else 0)
+    before = [a for a in alarms if mode < 0 or a <= mode]
+    assert last == (before[-1] if before else 0), (last, before)
+    assert len(alarms) >= 2
 
 
 def pin_greedy_after_switch(lib):
@@ -534,7 +583,8 @@ def pin_greedy_after_switch(lib):
         r_prev = np.array([r])
 
 
-ALL_PINS += [pin_page_hinkley_switch_round, pin_greedy_after_switch]
+ALL_PINS += [pin_page_hinkley_worked_example, pin_page_hinkley_threshold_is_strict,
+             pin_page_hinkley_switch_round, pin_greedy_after_switch]
 
 
 # ---- mixed-maturity refinement of the action space (Sec. 4.4) ----

@@ -44,9 +44,15 @@ MUTANTS = {
                                     "if (gone[k] && k <= o->cascade_k) kstar = k;"),
     "keep_one_worst_mean": ("(n[keep] == 0 || mean[k] > mean[keep])", "(n[keep] == 0 || mean[k] < mean[keep])"),
     "reward_sum_not_kept": ("    o->rsum[ik] += r;", "    o->rsum[ik] += 0.0 * r;"),
-    "ph_drift_sign": ("s[2] = s[2] + (r - s[1] - o->ph_delta);", "s[2] = s[2] + (r - s[1] + o->ph_delta);"),
-    "ph_minimum_not_tracked": ("s[3] = fminf(s[3], s[2]);", "s[3] = s[2];"),
-    "ph_no_restart": ("        for (int q = 0; q < 6; ++q) s[q] = 0.0f;\n", ""),
+    "ph_drift_sign": ("p->up += (r - rbar) - o->ph_delta;", "p->up += (r - rbar) + o->ph_delta;"),
+    "ph_minimum_not_tracked": ("if (p->up < p->up_min) p->up_min = p->up;", "p->up_min = p->up;"),
+    "ph_no_restart": ("        memset(p, 0, sizeof(*p));\n", ""),
+    "ph_mean_before_reward": ("const double rbar = p->sum / p->n;",
+                              "const double rbar = p->n > 1.0 ? (p->sum - r) / (p->n - 1.0) : 0.0;"),
+    "ph_one_sided": ("const double stat = fmax(p->up - p->up_min, p->dn - p->dn_min);",
+                     "const double stat = p->up - p->up_min;"),
+    "ph_alarm_inclusive": ("if (stat > o->ph_lambda) {", "if (stat >= o->ph_lambda) {"),
+    "ph_downward_sign": ("p->dn += (rbar - r) - o->ph_delta;", "p->dn += (r - rbar) - o->ph_delta;"),
     "ph_window_off_by_one": ("t - o->ph_last[i] >= o->ph_window", "t - o->ph_last[i] > o->ph_window"),
     "ph_min_rounds_ignored": ("t >= o->ph_min_rounds && ", ""),
     "greedy_scores_with_bonus": ("U[k] = greedy ? m : m + alpha * w;", "U[k] = m + alpha * w;"),

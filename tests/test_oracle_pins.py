@@ -47,3 +47,37 @@ def test_worked_example_is_self_consistent():
         assert Ai == ex["final_Ainv"][k]
         theta = [Ai[0][0] * b[k][0] + Ai[0][1] * b[k][1], Ai[1][0] * b[k][0] + Ai[1][1] * b[k][1]]
         assert theta == ex["final_theta"][k]
+
+
+def test_page_hinkley_example_is_self_consistent():
+    """The hand derivation's numbers agree with the test's definition redone
+    in exact rationals: each running mean recomputed from the rewards since
+    the last restart, the cumulative sums and their minima rebuilt from them
+    (catches typos in the fixture)."""
+    from fractions import Fraction as F
+    from golden_example import load_page_hinkley_example
+    ex = load_page_hinkley_example()
+    delta, lam = ex["delta"], ex["lambda"]
+    seg, last, mode = [], 0, -1
+    for rd in ex["rounds"]:
+        t = rd["t"]
+        if mode < 0:
+            seg.append(rd["r"])
+            sums = [F(0), F(0)]
+            mins = [F(0), F(0)]
+            for q in range(len(seg)):
+                rbar = sum(seg[:q + 1]) / (q + 1)
+                sums = [sums[0] + seg[q] - rbar - delta, sums[1] + rbar - seg[q] - delta]
+                mins = [min(mins[0], sums[0]), min(mins[1], sums[1])]
+            stat = max(sums[0] - mins[0], sums[1] - mins[1])
+            margin = lam - stat
+            alarm = int(stat > lam)
+            state = [F(len(seg)), sum(seg) / len(seg), sums[0], mins[0], sums[1], mins[1]]
+            if alarm:
+                last, seg, state = t, [], [F(0)] * 6
+            if t >= ex["min_rounds"] and t - last >= ex["window"]:
+                mode = t
+        else:
+            alarm = 0
+        assert rd["alarm"] == alarm and rd["mode"] == mode and rd["margin"] == margin, t
+        assert rd["state"] == state, (t, rd["state"], state)

@@ -47,7 +47,7 @@ def _record(cfg, X, R):
         for i in range(B):
             st, margin, last, mode = ora.page_hinkley(i)
             ph[t, i, 0] = mode
-            ph[t, i, 1:7] = st.view(np.int32)
+            ph[t, i, 1:7] = st.astype(np.float32).view(np.int32)
             ph[t, i, 7] = last
             ph[t, i, 8] = np.float32(margin).view(np.int32)
         r_prev = R[t]
@@ -78,8 +78,9 @@ def test_planted_difference_fails(plant):
         t = int(np.flatnonzero(ph[:, :, 7].max(axis=1) > 0)[0])
         j = int(np.flatnonzero(ph[t, :, 7] > 0)[0])
         ph[t:, j, 7] += 1
-    elif plant == "statistic":          # one ulp in the running mean
-        ph[t_sw // 2, i, 2] += 1
+    elif plant == "statistic":          # the running mean off by 1e-3
+        st = ph[t_sw // 2, i, 1:7].view(np.float32)
+        st[1] += np.float32(1e-3)
     else:                               # a greedy score off by 1e-3
         s[t_sw + 1, i, :, int(a[t_sw + 1, i])] += 1e-3
     with pytest.raises(parity.ParityError):
@@ -228,9 +229,9 @@ def _closed_record_full(wl):
         if wl.exploit:
             stats, margin, last, mode = o.page_hinkley_all()
             ph[t, :, 0] = mode
-            ph[t, :, 1:7] = stats.view(np.int32)
+            ph[t, :, 1:7] = stats.astype(np.float32).view(np.int32)
             ph[t, :, 7] = last
-            ph[t, :, 8] = margin.view(np.int32)
+            ph[t, :, 8] = margin.astype(np.float32).view(np.int32)
         win[t] = o.windows()
     out = run_closed_loop(wl, arrivals, noise, T=T, record=True,
                           on_create=lambda o: box.__setitem__("ora", o), on_commit=commit)
