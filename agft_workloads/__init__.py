@@ -7,10 +7,10 @@ defines sizes, constants and random draws that both the GPU path and the
 CPU oracle consume as inputs.
 """
 from .configs import (WORKLOADS, ENV, Workload, get_workload, arm_values, with_paper_pruning,
-                      with_exploitation, with_refinement, PAPER_PRUNING)
+                      with_exploitation, with_refinement, with_rule_one_reevaluated, PAPER_PRUNING)
 from .traces import exogenous, probe_instances
 
 __all__ = ["WORKLOADS", "ENV", "Workload", "get_workload", "arm_values", "with_paper_pruning",
-           "with_exploitation", "with_refinement",
+           "with_exploitation", "with_refinement", "with_rule_one_reevaluated",
            "PAPER_PRUNING",
            "exogenous", "probe_instances"]

@@ -33,6 +33,9 @@ class Workload:
     trace: str           # load-trace family, see traces.py
     drift: float = 0.0   # power/latency coefficients b, c scale to (1 + drift) at t = T - 1
     description: str = ""
+    # rule 1 removes arms for good (1), or is re-evaluated over the whole
+    # action space at each of its steps (0: the non-sticky reading)
+    prune_sticky: int = 1
     # the paper's pruning heuristics (rule bits 2, 4, 8; Sec. 4.3): the example
     # values the paper gives, plus a reading of the unstated ones
     # (tolerance multiplier and the minimum number of compared arms)
@@ -136,6 +139,16 @@ def with_exploitation(wl: Workload) -> Workload:
     return Workload(**d)
 
 
+def with_rule_one_reevaluated(wl: Workload) -> Workload:
+    """The same workload with rule 1 re-evaluated over every arm at each of
+    its steps instead of removing arms for good."""
+    d = dict(wl.__dict__)
+    d["prune_sticky"] = 0
+    d["name"] = wl.name + "n"
+    d["description"] = wl.description + ", rule 1 re-evaluated over every arm at each of its steps"
+    return Workload(**d)
+
+
 def with_refinement(wl: Workload) -> Workload:
     """The same workload with the mixed-maturity refinement of the action space."""
     d = dict(wl.__dict__)
@@ -153,9 +166,11 @@ def get_workload(cfg, **overrides) -> Workload:
         body = cfg.replace("cfg", "")
         suffix = body.lstrip("0123456789")
         cfg = int(body[:len(body) - len(suffix)])
-        if set(suffix) - set("per"):
+        if set(suffix) - set("pern"):
             raise ValueError(f"unknown workload suffix {suffix!r} (p: paper pruning, "
-                             f"e: exploitation, r: refinement)")
+                             f"e: exploitation, r: refinement, n: rule 1 re-evaluated)")
+        if "n" in suffix and "p" in suffix:
+            raise ValueError("the paper's rules remove arms for good: no re-evaluated rule 1 beside them")
     wl = WORKLOADS[cfg]
     if "p" in suffix:
         wl = with_paper_pruning(wl)
@@ -163,6 +178,8 @@ def get_workload(cfg, **overrides) -> Workload:
         wl = with_exploitation(wl)
     if "r" in suffix:
         wl = with_refinement(wl)
+    if "n" in suffix:
+        wl = with_rule_one_reevaluated(wl)
     if overrides:
         d = dict(wl.__dict__)
         d.update(overrides)

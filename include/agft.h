@@ -39,12 +39,13 @@
 extern "C" {
 #endif
 
-#define AGFT_ABI_VERSION 4
+#define AGFT_ABI_VERSION 5
 
 enum agft_status {
     AGFT_OK = 0,
     AGFT_E_INVAL = -1,       /* NULL pointer, size or value out of range */
-    AGFT_E_UNSUPPORTED = -2, /* well-formed but not supported (d not in {8,16,32}) */
+    AGFT_E_UNSUPPORTED = -2, /* well-formed but not supported (d not in {8,16,32}, a
+                                non-sticky rule 1 beside rules 2-8) */
     AGFT_E_STATE = -3,       /* call not valid now (missing reward, adopted
                                 buffer that does not match the configuration) */
     AGFT_E_HIP = -4          /* HIP runtime error, including earlier device faults */
@@ -60,7 +61,8 @@ typedef struct agft_config {
     float lambda;         /* ridge prior, A_k(0) = lambda I: finite, > 0 */
     float alpha0;         /* exploration weight of Eq. 1: finite, >= 0 */
     int32_t alpha_sched;  /* 0: alpha_t = alpha0; 1: alpha_t = alpha0 / sqrt(t + 1) */
-    int32_t prune_rule;   /* bit mask of pruning rules; every rule removes arms for good:
+    int32_t prune_rule;   /* bit mask of pruning rules; every rule removes arms for good
+                             (rule 1 unless prune_sticky is 0):
                              1  confidence bounds: at steps t > 0 with
                                 t % prune_period == 0, an active arm k goes when
                                 UCB_k < max_j LCB_j over the active arms j, with that
@@ -82,6 +84,14 @@ typedef struct agft_config {
                              if they would leave no arm, the arm with the best mean
                              reward (lowest index on ties) stays. */
     int32_t prune_period; /* period of rule 1; >= 1 */
+    int32_t prune_sticky; /* 1: rule 1 removes arms for good, like the paper's own rules
+                             (Sec. 4.3); 0: rule 1 is re-evaluated at each of its steps
+                             over the whole action space (every arm of it scored, the
+                             kept set {k : UCB_k >= max_j LCB_j} replacing the previous
+                             one), so an arm removed once can come back.  0 is supported
+                             with rule 1 alone (prune_rule 0 or 1; AGFT_E_UNSUPPORTED
+                             beside rules 2-8).  Must be 0 or 1: a zero-filled
+                             configuration gets the non-sticky reading. */
     uint32_t flags;       /* 0 or AGFT_ADOPT_STATE */
     /* parameters of rules 2, 4, 8 (read only when the rule's bit is set) */
     int32_t ext_rounds;    /* >= 0 */
@@ -158,7 +168,9 @@ typedef struct agft_state_view {
                            TF = 4, float TF*j+3 is 0).  Slots past K in the last
                            block hold zeros. */
     uint32_t *mask;     /* [B][mask_words]: bit k%32 of word k/32 set = arm k not
-                           removed by a pruning rule (the action space is apart) */
+                           removed by a pruning rule (the action space is apart; with
+                           a non-sticky rule 1, the arms its last evaluation kept and
+                           every arm it did not score) */
     int32_t *inst;      /* [B][inst_words] per-instance block of 32-bit words:
                            [0] last decision (-1: none), [1] arms in play (in the
                            action space and not removed by a rule),
@@ -166,7 +178,12 @@ typedef struct agft_state_view {
                            [3] -1 while exploring, else the round exploitation began,
                            [4..9] Page-Hinkley n, mean, m+, min m+, m-, min m- (fp32),
                            [10] round of its last alarm, [11] its last margin (fp32),
-                           [12] [13] [14] action space lo, hi, stride, [15] reserved,
+                           [12] [13] [14] action space lo, hi, stride,
+                           [15] top-two gap of the last decision made with a score
+                           dump (d_scores non-NULL): the largest score of the arms
+                           kept by pruning minus the second largest (fp32; 0 at a
+                           tie, +inf with one arm kept; the argmax margin of Eq. 1,
+                           or of Eq. 2 once exploiting),
                            [16 .. 16+d) context of the last decision (fp32) */
     int32_t inst_words; /* words per instance block: 16 + d rounded up to 16 */
     int32_t *stats;     /* [B][K][2] per arm: [0] rewards folded in (int32),
@@ -211,7 +228,9 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
  *           when a decision is pending (AGFT_E_STATE otherwise), else ignored.
  * d_action  [B] int32, device, or NULL.
  * d_scores  [B][2][K] fp32, device, or NULL: UCB (row 0) and LCB (row 1) of
- *           every arm active before this step's pruning, -inf for the others.
+ *           every arm active before this step's pruning, -inf for the others;
+ *           with it the step also leaves the top-two gap of its decision in
+ *           word 15 of each instance block (agft_state_view.inst).
  */
 int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t *d_action,
               float *d_scores);
@@ -233,7 +252,8 @@ typedef struct agft_launch_shape {
 } agft_launch_shape;
 
 /* Fill *out for cfg.  AGFT_E_INVAL if cfg is invalid or out is NULL,
- * AGFT_E_UNSUPPORTED for a context dimension other than 8, 16, 32. */
+ * AGFT_E_UNSUPPORTED for a context dimension other than 8, 16, 32 or a
+ * non-sticky rule 1 beside rules 2-8. */
 int agft_launch_shape_for(const agft_config *cfg, agft_launch_shape *out);
 
 /* Fill *out with device pointers into the state and the handle's counters. */

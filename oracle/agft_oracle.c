@@ -39,6 +39,13 @@
  * and 4 are judged together.  If they would leave no arm, the one with the
  * best mean reward (lowest index on ties) stays.
  *
+ * Non-sticky reading of rule 1 (ora_set_sticky(h, 0); rule 1 alone, no rule
+ * 2-8): at each of its steps rule 1 starts again from the whole action
+ * space instead of the arms still active, so the kept set is
+ * {k in space : UCB_k >= max over the space of LCB_j}, every arm of the space
+ * scored; between its steps that set stands.  An arm removed once can come
+ * back at a later rule-1 step.
+ *
  * The paper gives the update as Eq. 3-5: A and b are accumulated as written
  * and A_k^{-1} is recomputed by Gauss-Jordan elimination with partial
  * pivoting each time A_k changes; theta_k is then recomputed as A_k^{-1} b_k.
@@ -104,6 +111,7 @@ struct ph_test {
 
 typedef struct {
     int B, K, d, prune, period, sched;
+    int sticky;             /* 1: rule 1 removes for good; 0: re-evaluated over the space */
     double lambda, alpha0;
     /* parameters of rules 2-8 */
     int ext_rounds, ext_min_n, hist_after, hist_min_n, hist_min_arms, cascade_k;
@@ -192,7 +200,7 @@ void *ora_create(int B, int K, int d, double lambda, double alpha0, int sched,
     ora_t *o = (ora_t *)calloc(1, sizeof(ora_t));
     if (!o) return NULL;
     o->B = B; o->K = K; o->d = d; o->lambda = lambda; o->alpha0 = alpha0;
-    o->sched = sched; o->prune = prune; o->period = period;
+    o->sched = sched; o->prune = prune; o->period = period; o->sticky = 1;
     size_t nk = (size_t)B * K;
     o->A = (double *)calloc(nk * d * d, sizeof(double));
     o->b = (double *)calloc(nk * d, sizeof(double));
@@ -241,6 +249,12 @@ void ora_destroy(void *h)
     free(o->A); free(o->b); free(o->Ainv); free(o->theta); free(o->active);
     free(o->nsel); free(o->rsum); free(o->xprev); free(o->aprev); free(o->bad);
     free(o->ph); free(o->ph_margin); free(o->ph_last); free(o->mode); free(o->win); free(o);
+}
+
+/* Rule 1 sticky (1, the default) or re-evaluated at each of its steps (0). */
+void ora_set_sticky(void *h, int sticky)
+{
+    ((ora_t *)h)->sticky = sticky ? 1 : 0;
 }
 
 /* Refinement: on/off and its parameters (see the header); call before the
@@ -533,6 +547,14 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
             if (margins) memcpy(margins + (size_t)i * K, marg, sizeof(double) * K);
             continue;
         }
+        if (o->exploit && o->mode[i] < 0 && t >= o->ph_min_rounds && t - o->ph_last[i] >= o->ph_window)
+            o->mode[i] = t;
+        const int greedy = o->mode[i] >= 0;
+        if (prune_now && !o->sticky && !greedy)
+            for (int k = 0; k < K; ++k) {   /* rule 1 starts again from the whole space */
+                kp[k] = 1;
+                act0[k] = in_space(o, i, k);
+            }
         if (o->prune & 14) {
             heuristic_prune(o, i, t, act, act1, marg);
             for (int k = 0; k < K; ++k)
@@ -540,9 +562,6 @@ void ora_decide_ex(void *h, const double *x, const double *r, double *ucb, doubl
             act = act1;
         }
         if (margins) memcpy(margins + (size_t)i * K, marg, sizeof(double) * K);
-        if (o->exploit && o->mode[i] < 0 && t >= o->ph_min_rounds && t - o->ph_last[i] >= o->ph_window)
-            o->mode[i] = t;
-        const int greedy = o->mode[i] >= 0;
         for (int k = 0; k < K; ++k) {
             if (!act[k]) continue;
             size_t ik = (size_t)i * K + k;

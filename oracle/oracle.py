@@ -37,6 +37,7 @@ def _declare(lib):
     lib.ora_get_ph.argtypes = [P, I, P, P, P, P]
     lib.ora_set_ph.argtypes = [P, I, P, D, L, L]
     lib.ora_set_refine.argtypes = [P, I, I, I, I, I, I]
+    lib.ora_set_sticky.argtypes = [P, I]
     lib.ora_get_window.argtypes = [P, I, P, P, P]
     lib.ora_get_ph_all.argtypes = [P, P, P, P, P]
     lib.ora_get_window_all.argtypes = [P, P]
@@ -85,6 +86,8 @@ class Oracle:
     def from_workload(cls, wl, B=None, lib=None):
         o = cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0,
                 wl.alpha_sched, wl.prune, wl.period, lib=lib)
+        if not wl.prune_sticky:
+            o.set_sticky(False)
         if wl.prune & 14:
             o.set_heuristics(**wl.heuristics())
         if wl.exploit:
@@ -92,6 +95,11 @@ class Oracle:
         if wl.refine:
             o.set_refine(True, **wl.refinement())
         return o
+
+    def set_sticky(self, sticky):
+        """Rule 1 removes arms for good (True, the default) or is re-evaluated
+        over the whole action space at each of its steps (False)."""
+        self.lib.ora_set_sticky(self.h, int(bool(sticky)))
 
     def set_exploit(self, on, ph_delta, ph_lambda, ph_window, ph_min_rounds):
         """Page-Hinkley switch to greedy exploitation (Sec. 4.2, Eq. 2)."""

@@ -24,7 +24,7 @@ _i32, _u32, _f32, _i64, _sz, _vp = (ctypes.c_int32, ctypes.c_uint32, ctypes.c_fl
 class agft_config(ctypes.Structure):
     _fields_ = [("B", _i32), ("K", _i32), ("d", _i32), ("lambda_", _f32), ("alpha0", _f32),
                 ("alpha_sched", _i32), ("prune_rule", _i32), ("prune_period", _i32),
-                ("flags", _u32),
+                ("prune_sticky", _i32), ("flags", _u32),
                 ("ext_rounds", _i32), ("ext_min_n", _i32), ("ext_thr", _f32),
                 ("hist_after", _i32), ("hist_min_n", _i32), ("hist_kappa", _f32),
                 ("hist_min_arms", _i32), ("cascade_k", _i32),
@@ -55,7 +55,7 @@ class agft_launch_shape(ctypes.Structure):
     _fields_ = [("waves", _i32), ("simd_waves", _i32), ("tail_floats", _i32), ("early_update", _i32)]
 
 
-ABI_VERSION = 4   # AGFT_ABI_VERSION of the agft_config layout declared here
+ABI_VERSION = 5   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
             "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version", "agft_launch_shape_for",

@@ -179,12 +179,13 @@ __device__ inline void unpack(int e, int &i, int &j) {
 // Per-instance block of 32-bit words: previous action, active-arm count,
 // non-finite-input count, mode (-1 exploring, else the round exploitation
 // began), the Page-Hinkley state (n, mean, m+, min m+, m-, min m-), the round
-// of its last alarm, its last margin, the action space (lo, hi, stride), a
-// spare word, then the stashed context.  Kept together so the epilogue
+// of its last alarm, its last margin, the action space (lo, hi, stride), the
+// top-two score gap of the last decision that dumped its scores, then the
+// stashed context.  Kept together so the epilogue
 // writes one or two lines per instance.
 constexpr int kInstAprev = 0, kInstKact = 1, kInstBad = 2, kInstMode = 3, kInstPh = 4,
               kInstPhLast = 10, kInstPhMargin = 11, kInstLo = 12, kInstHi = 13, kInstStride = 14,
-              kInstX = 16;
+              kInstGap = 15, kInstX = 16;
 
 int inst_words(int d) { return (kInstX + d + 15) / 16 * 16; }
 
@@ -365,6 +366,7 @@ struct StepArgs {
     int32_t B, K, KW, IW;
     int32_t apply_update;  // a decision is pending
     int32_t prune_now;
+    int32_t prune_reset;   // rule 1 starts again from the whole action space (non-sticky)
     int32_t early_update;  // fold the previous reward in before the stream
     int32_t keep_stats;    // maintain the per-arm reward counts and sums
     float alpha;
@@ -453,20 +455,37 @@ __device__ __forceinline__ BestPair wave_best(BestPair b) {
     return b;
 }
 
-// Inclusive prefix sum over lanes 0..31 (DPP shifts within rows of 16, then
-// the first row's total added to the second row); lanes 32..63 unspecified.
-template <class T>
-__device__ __forceinline__ T scan32(T v) {
-    auto shr = [](T x, auto ctrl) {
-        const int xi = __builtin_bit_cast(int, x);
-        return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(0, xi, decltype(ctrl)::value, 0xF, 0xF, true));
+// Inclusive prefix sum within aligned segments of SEG lanes (8, 16 or 32):
+// DPP shifts within rows of 16 lanes (zero-filled at row edges), masked at
+// the edges of 8-lane segments; for 32 lanes, the first row's total is then
+// added to the second row of each half-wavefront.
+template <int SEG>
+__device__ __forceinline__ float segment_scan(float v, int lane) {
+    static_assert(SEG == 8 || SEG == 16 || SEG == 32, "segments of 8, 16 or 32 lanes");
+    auto shr = [](float x, auto ctrl) {
+        return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), decltype(ctrl)::value,
+                                                          0xF, 0xF, true));
     };
-    v += shr(v, std::integral_constant<int, 0x111>{});   // row_shr:1
-    v += shr(v, std::integral_constant<int, 0x112>{});   // row_shr:2
-    v += shr(v, std::integral_constant<int, 0x114>{});   // row_shr:4
-    v += shr(v, std::integral_constant<int, 0x118>{});   // row_shr:8
-    const int vi = __builtin_bit_cast(int, v);
-    v += __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(0, vi, 0x142, 0xA, 0xF, false));  // row_bcast:15
+    const int pos = lane & 7;
+    float s = shr(v, std::integral_constant<int, 0x111>{});    // row_shr:1
+    v += (SEG > 8 || pos >= 1) ? s : 0.0f;
+    s = shr(v, std::integral_constant<int, 0x112>{});          // row_shr:2
+    v += (SEG > 8 || pos >= 2) ? s : 0.0f;
+    s = shr(v, std::integral_constant<int, 0x114>{});          // row_shr:4
+    v += (SEG > 8 || pos >= 4) ? s : 0.0f;
+    if constexpr (SEG >= 16) v += shr(v, std::integral_constant<int, 0x118>{});   // row_shr:8
+    if constexpr (SEG == 32)
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xA, 0xF, false));  // row_bcast:15
+    return v;
+}
+
+// Sum over the 64/SEG segments of a wavefront: every lane ends with the
+// total of its column (lane % SEG) over the segments.
+template <int SEG>
+__device__ __forceinline__ float segment_colsum(float v) {
+    if constexpr (SEG == 8) v += dpp<0x128>(v);   // row_ror:8, the other half row
+    if constexpr (SEG <= 16) v += __shfl_xor(v, 16);
+    v += __shfl_xor(v, 32);
     return v;
 }
 
@@ -519,10 +538,7 @@ void agft_step_kernel(StepArgs p) {
 
     __shared__ float s_old[R::CAN];
     __shared__ float s_new[R::CAN];
-    __shared__ float s_f[D];
-    __shared__ float s_ca[D];
-    __shared__ float s_cb[D];
-    __shared__ float s_scal[2];   // alpha_{d-1}, prediction error
+    __shared__ float s_fpart[NW][D];   // per-wavefront partial sums of f = S^T xp
     // per-arm scores and the list of arms to stream, sized by K at launch
     // (step_lds_bytes) so that small arm counts leave room for more workgroups
     extern __shared__ float s_arm[];
@@ -543,6 +559,9 @@ void agft_step_kernel(StepArgs p) {
     __shared__ int2 s_stu;      // its arm's reward count and sum
 
     const bool decide = p.ctx != nullptr;
+    // the instance's mask words, issued first: they depend on nothing, and the
+    // list of arms to stream waits for them
+    const uint32_t raw_word = (wave == 0 && lane < KW) ? p.mask[(size_t)inst * KW + lane] : 0u;
 
     // Per-instance words, uniform over the workgroup (scalar loads at kernel
     // start): context, previous decision and its reward.  The previous
@@ -629,13 +648,14 @@ void agft_step_kernel(StepArgs p) {
         if (p.keep_stats && tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
     }
 
-    // the arms in play: not removed by a pruning rule, inside the action space
+    // the arms in play: not removed by a pruning rule, inside the action space;
+    // at a rule-1 step of the non-sticky reading, every arm of the space
     const int sp_lo = blk[kInstLo], sp_hi = blk[kInstHi];
     const int sp_st = blk[kInstStride] > 1 ? blk[kInstStride] : 1;
+    const bool reset = p.prune_reset && !greedy && x_ok;
     if (wave == 0 && lane < KW) {
-        const uint32_t raw = p.mask[(size_t)inst * KW + lane];
-        s_raw[lane] = raw;
-        s_mask[lane] = raw & space_bits(lane, sp_lo, sp_hi, sp_st);
+        s_raw[lane] = raw_word;
+        s_mask[lane] = (reset ? 0xffffffffu : raw_word) & space_bits(lane, sp_lo, sp_hi, sp_st);
     }
 
     // The paper's pruning rules (Sec. 4.3) on the arms active at step start,
@@ -821,42 +841,51 @@ void agft_step_kernel(StepArgs p) {
         if (upd) {
             const float *sth = s_old;         // theta
             const float *sS = s_old + D;      // packed factor
-            if (wave == 0) {
-                // f_j = sum_{i<=j} S_ij xp_i, alpha_j = 1 + f_0^2 + ... + f_j^2 (scan),
-                // column coefficients, prediction error r - xp^T theta
-                float fj = 0.0f;
+            // Lane l of every wavefront takes column j = l % D of one row per
+            // pass (row segments of D lanes; a pass of the workgroup covers RP
+            // rows), so that the column sums and the row prefix sums below are
+            // segment-wide DPP reductions instead of D-step loops on one lane.
+            constexpr int SEGS = kWave / D, RP = NW * SEGS, NP = (D + RP - 1) / RP;
+            const int jc = lane % D, seg = lane / D;
+            // f_j = sum_{i<=j} S_ij xp_i: this lane's rows, then the other
+            // segments of the wavefront, then the other wavefronts
+            float fj = 0.0f;
 #pragma unroll
-                for (int i = 0; i < D; ++i)
-                    if (i <= lane) fj = fmaf(sS[packed(i, lane < D ? lane : 0)], s_xp[i], fj);
-                if (lane >= D) fj = 0.0f;
-                const float incl = scan32(fj * fj);
-                float pred = lane < D ? s_xp[lane] * sth[lane] : 0.0f;
-                pred = wave_reduce(pred, [](float a, float b) { return a + b; });
-                if (lane < D) {
-                    const float al = 1.0f + incl;
-                    const float al_prev = 1.0f + (incl - fj * fj);
-                    s_f[lane] = fj;
-                    s_ca[lane] = sqrtf(al_prev / al);
-                    s_cb[lane] = fj / sqrtf(al_prev * al);
-                    if (lane == D - 1) s_scal[0] = al;
-                }
-                if (lane == 0) s_scal[1] = r - pred;
+            for (int ps = 0; ps < NP; ++ps) {
+                const int i = ps * RP + wave * SEGS + seg;
+                if (i < D && i <= jc) fj = fmaf(sS[packed(i, jc)], s_xp[i], fj);
             }
-            __syncthreads();
-            if (wave == 0 && lane < D) {
-                // row i of S' = S M:  S'_ij = ca_j S_ij - cb_j g,  g = sum_{i<=q<j} f_q S_iq;
-                // the final g is (S f)_i, so the gain is g / alpha_{d-1}
-                const int i = lane;
-                float g = 0.0f;
+            fj = segment_colsum<D>(fj);
+            if constexpr (NW > 1) {
+                if (seg == 0) s_fpart[wave][jc] = fj;
+                __syncthreads();
+                fj = s_fpart[0][jc];
 #pragma unroll
-                for (int jc = 0; jc < D; ++jc) {
-                    if (jc >= i) {
-                        const float sij = sS[packed(i, jc)];
-                        s_new[D + packed(i, jc)] = s_ca[jc] * sij - s_cb[jc] * g;
-                        g = fmaf(s_f[jc], sij, g);
-                    }
-                }
-                s_new[i] = fmaf(g / s_scal[0], s_scal[1], sth[i]);
+                for (int w = 1; w < NW; ++w) fj += s_fpart[w][jc];
+            }
+            // alpha_j = 1 + f_0^2 + ... + f_j^2 (prefix over the segment) and the
+            // column coefficients of M; alpha_{d-1} from the segment's last lane
+            const float incl = segment_scan<D>(fj * fj, lane);
+            const float al = 1.0f + incl;
+            const float al_prev = 1.0f + (incl - fj * fj);
+            const float ca = sqrtf(al_prev / al), cb = fj / sqrtf(al_prev * al);
+            const float al_last = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(al), D - 1));
+            // prediction error r - xp^T theta
+            float pred = lane < D ? s_xp[lane] * sth[lane] : 0.0f;
+            pred = wave_reduce(pred, [](float a, float b) { return a + b; });
+            const float err = r - pred;
+            // row i of S' = S M:  S'_ij = ca_j S_ij - cb_j g_ij with g_ij the
+            // exclusive prefix sum of f_q S_iq along the row; its total is
+            // (S f)_i, so the gain is that total / alpha_{d-1}
+#pragma unroll
+            for (int ps = 0; ps < NP; ++ps) {
+                const int i = ps * RP + wave * SEGS + seg;
+                const bool in_row = i < D && i <= jc;
+                const float sij = in_row ? sS[packed(i, jc)] : 0.0f;
+                const float q = fj * sij;
+                const float qi = segment_scan<D>(q, lane);
+                if (in_row) s_new[D + packed(i, jc)] = ca * sij - cb * (qi - q);
+                if (i < D && jc == D - 1) s_new[i] = fmaf(qi / al_last, err, sth[i]);
             }
             __syncthreads();
             float4 *dst = p.arms + (size_t)inst * inst_chunks;
@@ -884,7 +913,9 @@ void agft_step_kernel(StepArgs p) {
             blk[kInstBad] += 1;
         }
     };
-    const bool early = p.early_update && !greedy;   // an exploiting instance has no pass in flight
+    // An exploiting instance has no pass in flight.  Where the whole list fits
+    // in the first pass, no later pass can wait behind the update.
+    const bool early = (p.early_update || nlist <= apw) && !greedy;
     if (early) update(cmap);
 
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
@@ -1041,14 +1072,19 @@ void agft_step_kernel(StepArgs p) {
     const bool stat_anchor = p.rf.now && p.rf.stat;
     int n = 0;
     float *sc = p.scores != nullptr ? p.scores + (size_t)inst * 2 * K : nullptr;
+    float top1 = -INFINITY, top2 = -INFINITY;   // two largest kept scores (with the dump only)
     for (int base = 0; base < K; base += nthr) {
         const int k = base + tid;
         const bool act = is_active(k);
         const float u = act ? s_ucb[k] : -INFINITY;
         const bool keep = act && !(u < lstar);
+        n += __popcll(__ballot(keep));   // uniform over the wavefront
         if (keep) {
             b = better(b, BestPair{u, k});
-            ++n;
+            if (sc != nullptr) {
+                top2 = fmaxf(top2, fminf(top1, u));
+                top1 = fmaxf(top1, u);
+            }
             if (stat_anchor) {
                 // best mean reward among the arms with enough rewards (this
                 // step's update already counted)
@@ -1061,23 +1097,46 @@ void agft_step_kernel(StepArgs p) {
             sc[K + k] = act ? s_lcb[k] : -INFINITY;
         }
         if (prune_now) {
-            // clear the arms rule 1 removed from the global words
+            // clear the arms rule 1 removed from the global words (non-sticky:
+            // the words become exactly this step's removals, all other arms set)
             const unsigned long long bal = __ballot(keep);
             const int w0 = (base + wave * kWave) >> 5;
             uint32_t *mwo = p.mask + (size_t)inst * KW;
+            auto all_arms = [&](int w) {
+                return K - 32 * w >= 32 ? 0xffffffffu : (1u << (K - 32 * w)) - 1u;
+            };
             if (lane == 0 && w0 < KW) {
-                s_raw[w0] &= ~(s_mask[w0] & ~(uint32_t)(bal & 0xffffffffull));
+                const uint32_t from = reset ? all_arms(w0) : s_raw[w0];
+                s_raw[w0] = from & ~(s_mask[w0] & ~(uint32_t)(bal & 0xffffffffull));
                 mwo[w0] = s_raw[w0];
             }
             if (lane == 0 && w0 + 1 < KW) {
-                s_raw[w0 + 1] &= ~(s_mask[w0 + 1] & ~(uint32_t)(bal >> 32));
+                const uint32_t from = reset ? all_arms(w0 + 1) : s_raw[w0 + 1];
+                s_raw[w0 + 1] = from & ~(s_mask[w0 + 1] & ~(uint32_t)(bal >> 32));
                 mwo[w0 + 1] = s_raw[w0 + 1];
             }
         }
     }
     b = wave_best(b);
-    n = wave_reduce(n, [](int a, int c) { return a + c; });
     if (stat_anchor) sb = wave_best(sb);
+    __shared__ float s_top[kMaxWaves][2];
+    if (sc != nullptr) {
+        // the two largest of a pair of (largest, second) pairs
+        auto merge = [&](float o1, float o2) {
+            top2 = fmaxf(fminf(top1, o1), fmaxf(top2, o2));
+            top1 = fmaxf(top1, o1);
+        };
+        merge(partner<0>(top1), partner<0>(top2));
+        merge(partner<1>(top1), partner<1>(top2));
+        merge(partner<2>(top1), partner<2>(top2));
+        merge(partner<3>(top1), partner<3>(top2));
+        merge(partner<4>(top1), partner<4>(top2));
+        merge(partner<5>(top1), partner<5>(top2));
+        if (lane == 0) {
+            s_top[wave][0] = top1;
+            s_top[wave][1] = top2;
+        }
+    }
     if (lane == 0) {
         s_red_v[wave] = b.v;
         s_red_k[wave] = b.k;
@@ -1125,6 +1184,14 @@ void agft_step_kernel(StepArgs p) {
         }
         if (lane == kInstAprev) blk[kInstAprev] = a;
         if (lane == kInstKact) blk[kInstKact] = cnt;
+        if (sc != nullptr && lane == kInstGap) {
+            float t1 = s_top[0][0], t2 = s_top[0][1];
+            for (int w = 1; w < nwave; ++w) {
+                t2 = fmaxf(fminf(t1, s_top[w][0]), fmaxf(t2, s_top[w][1]));
+                t1 = fmaxf(t1, s_top[w][0]);
+            }
+            blk[kInstGap] = __float_as_int(t1 - t2);   // +inf with one kept arm
+        }
         if (anchor >= 0 && lane >= kInstLo && lane <= kInstStride)
             blk[lane] = lane == kInstLo ? nlo : (lane == kInstHi ? nhi : 1);
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
@@ -1248,6 +1315,7 @@ bool config_ok(const agft_config *c) {
     if (c->alpha_sched != 0 && c->alpha_sched != 1) return false;
     if (c->prune_rule < 0 || c->prune_rule > 15) return false;
     if (c->prune_period < 1) return false;
+    if (c->prune_sticky != 0 && c->prune_sticky != 1) return false;
     if ((c->prune_rule & 2) && (c->ext_rounds < 0 || c->ext_min_n < 1 || !std::isfinite(c->ext_thr)))
         return false;
     if ((c->prune_rule & 4) && (c->hist_after < 0 || c->hist_min_n < 1 || c->hist_min_arms < 1 ||
@@ -1266,7 +1334,12 @@ bool config_ok(const agft_config *c) {
     return true;
 }
 
-bool dim_supported(int d) { return d == 8 || d == 16 || d == 32; }
+// Context dimensions the kernels are built for; a non-sticky rule 1 only on
+// its own (the paper's rules 2-8 remove arms for good, and one mask cannot
+// hold both kinds of removal).
+bool supported(const agft_config *c) {
+    return (c->d == 8 || c->d == 16 || c->d == 32) && (c->prune_sticky || !(c->prune_rule & 14));
+}
 
 int hip_status(hipError_t e) { return e == hipSuccess ? AGFT_OK : AGFT_E_HIP; }
 
@@ -1313,7 +1386,7 @@ void launch_step(int waves, unsigned grid, size_t lds, hipStream_t stream, const
 extern "C" {
 
 size_t agft_state_bytes(const agft_config *cfg) {
-    if (!config_ok(cfg) || !dim_supported(cfg->d)) return 0;
+    if (!config_ok(cfg) || !supported(cfg)) return 0;
     return layout_for(*cfg).total;
 }
 
@@ -1321,7 +1394,7 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
     if (out == nullptr) return AGFT_E_INVAL;
     *out = nullptr;
     if (!config_ok(cfg) || d_state == nullptr) return AGFT_E_INVAL;
-    if (!dim_supported(cfg->d)) return AGFT_E_UNSUPPORTED;
+    if (!supported(cfg)) return AGFT_E_UNSUPPORTED;
     if (reinterpret_cast<uintptr_t>(d_state) % kAlign != 0) return AGFT_E_INVAL;
     const Layout lay = layout_for(*cfg);
     if (nbytes < lay.total) return AGFT_E_INVAL;
@@ -1427,6 +1500,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
     p.apply_update = h->pending;
     const int64_t t = h->t;
     p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
+    p.prune_reset = p.prune_now && !c.prune_sticky ? 1 : 0;
     p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
     p.t_next = d_ctx != nullptr ? t + 1 : t;
     agft_launch_shape shape;
@@ -1468,7 +1542,7 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
 
 int agft_launch_shape_for(const agft_config *cfg, agft_launch_shape *out) {
     if (out == nullptr || !config_ok(cfg)) return AGFT_E_INVAL;
-    if (!dim_supported(cfg->d)) return AGFT_E_UNSUPPORTED;
+    if (!supported(cfg)) return AGFT_E_UNSUPPORTED;
     out->waves = waves_for(*cfg);
     out->tail_floats = tail_floats(*cfg);
     out->simd_waves = occupancy_for(*cfg, out->tail_floats);

@@ -12,7 +12,9 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
 
     arrivals, noise: [T+1][B] (numpy or torch) exogenous draws.
     probes: instance indices to record at every step (contexts, rewards,
-    actions, scores, masks); the records are returned as host tensors.
+    actions, masks, test words, action spaces; with scores, the scores and
+    the top-two gap of each decision); the records are returned as host
+    tensors.
     """
     T = wl.T if T is None else int(T)
     dev = torch.device(device)
@@ -35,6 +37,7 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
                    win=torch.empty(T, P, 3, dtype=torch.int32, device=dev))
         if scores:
             rec["scores"] = torch.empty(T, P, 2, wl.K, device=dev)
+            rec["gap"] = torch.empty(T, P, device=dev)
         view = tuner.view()
     x = env.reset()
     r = None
@@ -49,6 +52,7 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
             rec["win"][t] = view["window"].index_select(0, pidx)
             if scores:
                 rec["scores"][t] = sc.index_select(0, pidx)
+                rec["gap"][t] = view["gap"].index_select(0, pidx)
         r, x = env.step(t, action)
         if rec is not None:
             rec["r"][t] = r.index_select(0, pidx)

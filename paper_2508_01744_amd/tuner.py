@@ -16,10 +16,11 @@ def _stream_handle(stream):
 
 
 def make_config(B, K, d, lam=1.0, alpha0=1.0, alpha_sched=0, prune_rule=0, prune_period=50,
-                adopt=False, heuristics=None, exploit=None, refine=None):
+                adopt=False, heuristics=None, exploit=None, refine=None, prune_sticky=1):
     """The agft_config of a tuner (no device work)."""
     cfg = L.agft_config(int(B), int(K), int(d), float(lam), float(alpha0), int(alpha_sched),
-                        int(prune_rule), int(prune_period), L.AGFT_ADOPT_STATE if adopt else 0)
+                        int(prune_rule), int(prune_period), int(prune_sticky),
+                        L.AGFT_ADOPT_STATE if adopt else 0)
     for name, value in (heuristics or {}).items():
         setattr(cfg, name, value)
     if exploit:
@@ -38,7 +39,7 @@ def workload_config(wl, B=None):
     return make_config(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0, wl.alpha_sched,
                        wl.prune, wl.period, heuristics=wl.heuristics(),
                        exploit=wl.page_hinkley() if wl.exploit else None,
-                       refine=wl.refinement() if wl.refine else None)
+                       refine=wl.refinement() if wl.refine else None, prune_sticky=wl.prune_sticky)
 
 
 def launch_shape(cfg):
@@ -54,12 +55,12 @@ class Tuner:
 
     def __init__(self, B, K, d, lam=1.0, alpha0=1.0, alpha_sched=0, prune_rule=0,
                  prune_period=50, device="cuda", stream=None, state=None, adopt=False,
-                 heuristics=None, exploit=None, refine=None):
+                 heuristics=None, exploit=None, refine=None, prune_sticky=1):
         self.device = torch.device(device)
         if self.device.type == "cuda" and self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
         self.cfg = make_config(B, K, d, lam, alpha0, alpha_sched, prune_rule, prune_period, adopt,
-                               heuristics, exploit, refine)
+                               heuristics, exploit, refine, prune_sticky)
         self.nbytes = L.agft_state_bytes(self.cfg)
         if self.nbytes == 0:
             raise ValueError("invalid tuner configuration")
@@ -84,7 +85,7 @@ class Tuner:
         return cls(wl.B if B is None else B, wl.K, wl.d, wl.lam, wl.alpha0, wl.alpha_sched,
                    wl.prune, wl.period, heuristics=wl.heuristics(),
                    exploit=wl.page_hinkley() if wl.exploit else None,
-                   refine=wl.refinement() if wl.refine else None, **kw)
+                   refine=wl.refinement() if wl.refine else None, prune_sticky=wl.prune_sticky, **kw)
 
     def close(self):
         if getattr(self, "h", None):
@@ -152,7 +153,8 @@ class Tuner:
             mask=region(v.mask, B * KW, torch.int32, (B, KW)),
             inst=inst,
             aprev=inst[:, 0], kact=inst[:, 1], bad=inst[:, 2], mode=inst[:, 3], ph=inst[:, 3:12],
-            window=inst[:, 12:15], xprev=inst[:, 16:16 + d].view(torch.float32),
+            window=inst[:, 12:15], gap=inst[:, 15].view(torch.float32),
+            xprev=inst[:, 16:16 + d].view(torch.float32),
             stats=region(v.stats, B * K * 2, torch.int32, (B, K, 2)),
             theta=region(v.theta, B * K * d, torch.float32, (B, K, d)) if v.theta else None,
         )

@@ -53,6 +53,7 @@ int main(int argc, char **argv)
     cfg.alpha_sched = 0;
     cfg.prune_rule = 1;
     cfg.prune_period = 10;
+    cfg.prune_sticky = 1;
     const size_t nbytes = agft_state_bytes(&cfg);
     if (nbytes == 0) {
         fprintf(stderr, "invalid configuration\n");

@@ -17,12 +17,14 @@ def run_open_loop(cfg, X, R, flush=True):
     """Drive a Tuner with given contexts X [T][B][d] and rewards R [T][B].
     Returns host arrays: actions [T][B], mask words [T][B][KW], scores
     [T][B][2][K], the tuner, and a dict of the Page-Hinkley words [T][B][9]
-    ("ph") and the action spaces [T][B][3] ("win") after each step."""
+    ("ph"), the action spaces [T][B][3] ("win") and the top-two gaps [T][B]
+    ("gap") after each step."""
     T, B, d = X.shape
     dev = torch.device("cuda")
     tuner = Tuner(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
                   cfg["prune"], cfg["period"], device=dev, heuristics=cfg.get("heuristics"),
-                  exploit=cfg.get("exploit"), refine=cfg.get("refine"))
+                  exploit=cfg.get("exploit"), refine=cfg.get("refine"),
+                  prune_sticky=cfg.get("sticky", 1))
     Xd = torch.as_tensor(np.asarray(X, dtype=np.float32), device=dev)
     Rd = torch.as_tensor(np.asarray(R, dtype=np.float32), device=dev)
     K, KW = cfg["K"], (cfg["K"] + 31) // 32
@@ -31,17 +33,19 @@ def run_open_loop(cfg, X, R, flush=True):
     scores = torch.empty(T, B, 2, K, device=dev)
     ph = torch.empty(T, B, 9, dtype=torch.int32, device=dev)
     win = torch.empty(T, B, 3, dtype=torch.int32, device=dev)
+    gap = torch.empty(T, B, device=dev)
     view = tuner.view()
     for t in range(T):
         tuner.step(Xd[t], Rd[t - 1] if t > 0 else None, acts[t], scores[t])
         masks[t].copy_(view["mask"])
         ph[t].copy_(view["ph"])
         win[t].copy_(view["window"])
+        gap[t].copy_(view["gap"])
     if flush and T > 0:
         tuner.flush(Rd[T - 1])
     torch.cuda.synchronize()
     return (acts.cpu().numpy(), masks.cpu().numpy(), scores.cpu().numpy().astype(np.float64), tuner,
-            dict(ph=ph.cpu().numpy(), win=win.cpu().numpy()))
+            dict(ph=ph.cpu().numpy(), win=win.cpu().numpy(), gap=gap.cpu().numpy().astype(np.float64)))
 
 
 def random_contexts(seed, T, B, d, scale=1.0):

@@ -37,37 +37,45 @@ def _brute_scores(hist, lam, d, x, alpha):
     return A, b, theta, theta @ x + alpha * w, theta @ x - alpha * w
 
 
-def _brute_trajectory(lib, B, K, d, T, lam, alpha0, sched, prune, period, seed):
+def _brute_trajectory(lib, B, K, d, T, lam, alpha0, sched, prune, period, seed, sticky=True):
     """Drive the oracle with random contexts and rewards and check every
-    decision against brute force (explicit history, np.linalg, plain loops)."""
+    decision against brute force (explicit history, np.linalg, plain loops).
+    sticky=False: rule 1 re-evaluated at each of its steps over every arm.
+    Returns the number of arms that came back after rule 1 removed them."""
     rng = np.random.default_rng(seed)
     xs = _rand_contexts(rng, T, B, d)
     rs = rng.uniform(-2.0, 0.0, size=(T, B))
     ora = Oracle(B, K, d, lam, alpha0, sched, prune, period, lib=lib)
+    if not sticky:
+        ora.set_sticky(False)
     hist = [[[] for _ in range(K)] for _ in range(B)]
     active = np.ones((B, K), dtype=bool)
+    returned = 0
     r_prev = None
     for t in range(T):
         ucb, lcb, keep, action = ora.decide(xs[t], r_prev)
         alpha = alpha0 if sched == 0 else alpha0 / math.sqrt(t + 1.0)
+        prune_step = prune and t > 0 and t % period == 0
         for i in range(B):
+            scored = active[i] | (prune_step and not sticky)
             U = np.full(K, -np.inf)
             L = np.full(K, -np.inf)
             for k in range(K):
-                if active[i, k]:
+                if scored[k]:
                     _, _, _, U[k], L[k] = _brute_scores(hist[i][k], lam, d, xs[t, i], alpha)
             for k in range(K):
-                if active[i, k]:
+                if scored[k]:
                     assert abs(ucb[i, k] - U[k]) <= 1e-9 * max(1.0, abs(U[k])), (t, i, k)
                     assert abs(lcb[i, k] - L[k]) <= 1e-9 * max(1.0, abs(L[k])), (t, i, k)
                 else:
                     assert ucb[i, k] == -np.inf
             new_active = active[i].copy()
-            if prune and t > 0 and t % period == 0:
-                lstar = max(L[k] for k in range(K) if active[i, k])
+            if prune_step:
+                lstar = max(L[k] for k in range(K) if scored[k])
                 for k in range(K):
-                    if active[i, k] and U[k] < lstar:
-                        new_active[k] = False
+                    if scored[k]:
+                        new_active[k] = not U[k] < lstar
+                returned += int((new_active & ~active[i]).sum())
             assert (keep[i] == new_active).all(), (t, i)
             best = -1
             for k in range(K):
@@ -90,6 +98,7 @@ def _brute_trajectory(lib, B, K, d, T, lam, alpha0, sched, prune, period, seed):
             assert np.abs(st["theta"][k] - theta).max() <= 1e-10 * max(1.0, np.abs(theta).max())
             assert st["nsel"][k] == len(hist[i][k])
         assert (st["active"] == active[i]).all()
+    return returned
 
 
 def pin_brute_force_small(lib):
@@ -102,6 +111,49 @@ def pin_brute_force_small(lib):
                       period=5, seed=3)
     _brute_trajectory(lib, B=1, K=4, d=8, T=64, lam=1.0, alpha0=0.3, sched=0, prune=1,
                       period=4, seed=4)
+
+
+def pin_nonsticky_rule_one(lib):
+    """Rule 1 re-evaluated at each of its steps (the non-sticky reading):
+    the kept set is recomputed from every arm with that step's scores, so an
+    arm removed at one step can come back at a later one; the same brute
+    force as above, also with the refinement's moving action space."""
+    n = _brute_trajectory(lib, B=3, K=6, d=2, T=80, lam=1.0, alpha0=0.8, sched=0, prune=1,
+                          period=4, seed=31, sticky=False)
+    n += _brute_trajectory(lib, B=2, K=5, d=4, T=60, lam=0.5, alpha0=1.5, sched=1, prune=1,
+                           period=3, seed=32, sticky=False)
+    assert n > 0, "no removed arm came back"
+    _brute_refine_trajectory(lib, B=2, K=14, d=2, T=60, stride=3, half=2, period=5, mature=20,
+                             min_n=2, prune=1, pperiod=3, seed=33, sticky=False)
+    # once exploiting, rule 1 no longer runs: the kept set stands at its steps
+    e = Oracle(1, 6, 2, 1.0, 0.1, 0, 1, 4, lib=lib)
+    e.set_sticky(False)
+    e.set_exploit(True, ph_delta=0.05, ph_lambda=1e9, ph_window=10, ph_min_rounds=10)
+    rng = np.random.default_rng(36)
+    xs = _rand_contexts(rng, 40, 1, 2)
+    r = None
+    kept = None
+    for t in range(40):
+        u, l, k, a = e.step(xs[t], r)
+        if t == 9:
+            assert k[0].sum() == 2                 # rule 1 removed arms while exploring
+        if t >= 10:
+            assert np.array_equal(u, l)            # Eq. 2 scores
+            kept = k[0] if kept is None else kept
+            assert np.array_equal(k[0], kept), t   # and no rule-1 step touches the set
+        r = rng.uniform(-2.0, 0.0, size=1)
+    # up to the first rule-1 step both readings coincide
+    a = Oracle(2, 5, 2, 1.0, 0.8, 0, 1, 6, lib=lib)
+    b = Oracle(2, 5, 2, 1.0, 0.8, 0, 1, 6, lib=lib)
+    b.set_sticky(False)
+    rng = np.random.default_rng(34)
+    xs = _rand_contexts(rng, 7, 2, 2)
+    r = None
+    for t in range(7):
+        ua, _, ka, aa = a.step(xs[t], r)
+        ub, _, kb, ab = b.step(xs[t], r)
+        assert np.array_equal(ua, ub) and np.array_equal(ka, kb) and np.array_equal(aa, ab), t
+        r = rng.uniform(-2.0, 0.0, size=2)
 
 
 def pin_repeated_update_closed_form(lib):
@@ -296,7 +348,7 @@ def pin_convergence_linear_reward(lib):
     assert regret[T // 2:].sum() < regret[:T // 2].sum()
 
 
-ALL_PINS = [pin_brute_force_small, pin_repeated_update_closed_form, pin_ridge_least_squares,
+ALL_PINS = [pin_brute_force_small, pin_nonsticky_rule_one, pin_repeated_update_closed_form, pin_ridge_least_squares,
             pin_rational_worked_example, pin_textbook_reductions, pin_prune_invariants,
             pin_convergence_linear_reward]
 
@@ -594,19 +646,22 @@ def _in_space(k, lo, hi, stride):
 
 
 def _brute_refine_trajectory(lib, B, K, d, T, stride, half, period, mature, min_n, prune, pperiod,
-                             seed, alpha0=0.6):
+                             seed, alpha0=0.6, sticky=True):
     """Drive the oracle with refinement on and check every step against an
     independent restatement: the action space as an explicit set, scores by
     direct solve from each arm's full history (models persist while an arm is
     outside the space), rule 1, the argmax, and the anchor chosen after the
     decision (best mean reward with enough samples before maturity, the
-    decision itself after).  Returns the number of arms that re-entered the
-    space with a history of their own."""
+    decision itself after).  sticky=False: rule 1 re-evaluated at each of its
+    steps over the whole action space.  Returns the number of arms that
+    re-entered the space with a history of their own."""
     rng = np.random.default_rng(seed)
     xs = _rand_contexts(rng, T, B, d)
     rs = rng.uniform(-2.0, 0.0, size=(T, B))
     ora = Oracle(B, K, d, 1.0, alpha0, 0, prune, pperiod, lib=lib)
     ora.set_refine(True, period, stride, half, mature, min_n)
+    if not sticky:
+        ora.set_sticky(False)
     hist = [[[] for _ in range(K)] for _ in range(B)]
     pruned = np.zeros((B, K), dtype=bool)
     win = [(0, K - 1, stride) for _ in range(B)]
@@ -617,7 +672,8 @@ def _brute_refine_trajectory(lib, B, K, d, T, stride, half, period, mature, min_
         ucb, lcb, keep, action = ora.decide(xs[t], r_prev)
         for i in range(B):
             lo, hi, st = win[i]
-            space = [k for k in range(K) if _in_space(k, lo, hi, st) and not pruned[i, k]]
+            reeval = prune and t > 0 and t % pperiod == 0 and not sticky
+            space = [k for k in range(K) if _in_space(k, lo, hi, st) and (reeval or not pruned[i, k])]
             for k in range(K):
                 if k in space:
                     if seen_out[i, k] and hist[i][k]:
@@ -633,6 +689,8 @@ def _brute_refine_trajectory(lib, B, K, d, T, stride, half, period, mature, min_
             if prune and t > 0 and t % pperiod == 0:
                 lstar = max(lcb[i, k] for k in space)
                 survivors = [k for k in space if not ucb[i, k] < lstar]
+                if reeval:
+                    pruned[i] = False
                 for k in space:
                     if k not in survivors:
                         pruned[i, k] = True

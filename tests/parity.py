@@ -59,8 +59,11 @@ class ParityError(AssertionError):
 
 class Checker:
     def __init__(self, name, K, ids, g_a, g_keep, g_s=None, g_x=None, g_r=None, rules=0,
-                 cascade_k=0, g_ph=None, g_win=None, refine=None):
+                 cascade_k=0, g_ph=None, g_win=None, refine=None, g_gap=None):
         self.name, self.K, self.ids = name, K, list(ids)
+        # g_gap [T][n]: top-two gap of each decision (largest kept score minus
+        # the second), checked against the oracle's within both scores' tolerance
+        self.g_gap = g_gap
         self.g_a, self.g_keep, self.g_s, self.g_x, self.g_r = g_a, g_keep, g_s, g_x, g_r
         self.rules, self.cascade_k = rules, cascade_k
         # g_ph [T][n][9] int32: mode, Page-Hinkley n, mean, m+, min m+, m-, min m-,
@@ -73,7 +76,7 @@ class Checker:
         self.st = dict(max_score_err=0.0, max_ctx_err=0.0, max_reward_err=0.0, forced=0,
                        forced_prune=0, forced_rules=0, exact_tie_steps=0, decisions=0,
                        no_decision=0, max_ph_err=0.0, forced_ph=0, forced_mode=0,
-                       greedy_decisions=0, refinements=0, forced_window=0)
+                       greedy_decisions=0, refinements=0, forced_window=0, max_gap_err=0.0)
 
     def _anchor(self, lo, hi):
         h = self.refine["refine_half"]
@@ -231,6 +234,19 @@ class Checker:
                 st["exact_tie_steps"] += 1
                 if ga != own:
                     self.fail(f"exact tie broken wrongly at t={t}, instance {ids[i]}: {ga} vs {own}")
+            if self.g_gap is not None:
+                top = np.sort(u[np.isfinite(u)])[::-1]
+                o_gap = top[0] - top[1] if top.size > 1 else np.inf
+                g_gap = float(self.g_gap[t, i])
+                if np.isinf(o_gap):
+                    ok = np.isinf(g_gap) and g_gap > 0
+                    err = 0.0
+                else:
+                    err = abs(g_gap - o_gap) / max(1.0, abs(ustar))
+                    ok = err <= 2 * SCORE_TOL
+                st["max_gap_err"] = max(st["max_gap_err"], err)
+                if not ok:
+                    self.fail(f"top-two gap differs at t={t}, instance {ids[i]}: GPU {g_gap}, oracle {o_gap}")
             if ga != own:
                 st["forced"] += 1
             commit_a[i] = ga
@@ -475,7 +491,8 @@ def compare(wl, T, probes, rec):
                   rules=wl.prune, cascade_k=wl.cascade_k,
                   g_ph=rec["ph"].numpy() if wl.exploit else None,
                   g_win=rec["win"].numpy() if wl.refine else None,
-                  refine=wl.refinement() if wl.refine else None)
+                  refine=wl.refinement() if wl.refine else None,
+                  g_gap=rec["gap"].numpy().astype(np.float64) if "gap" in rec else None)
     out = run_closed_loop(wl, arrivals, noise, T=T, on_decide=chk, margins=bool(wl.prune & 14),
                           on_create=chk.bind, on_commit=chk.after_commit)
     st = chk.finish()
@@ -483,7 +500,7 @@ def compare(wl, T, probes, rec):
     return st
 
 
-def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None, g_win=None):
+def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None, g_win=None, g_gap=None):
     """Open loop: contexts X [T][B][d] and rewards R [T][B] (reward of the
     decision at t) given to both sides.  cfg: dict(B, K, d, lam, alpha0,
     sched, prune, period[, heuristics][, exploit][, refine]).  GPU records:
@@ -493,6 +510,8 @@ def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None, g_win=None)
     T = X.shape[0]
     ora = Oracle(cfg["B"], cfg["K"], cfg["d"], cfg["lam"], cfg["alpha0"], cfg["sched"],
                  cfg["prune"], cfg["period"])
+    if not cfg.get("sticky", 1):
+        ora.set_sticky(False)
     heur = cfg.get("heuristics")
     if heur:
         ora.set_heuristics(**heur)
@@ -505,7 +524,7 @@ def compare_open_loop(name, cfg, X, R, g_a, g_masks, g_s, g_ph=None, g_win=None)
     chk = Checker(name, cfg["K"], range(cfg["B"]), g_a, mask_words_to_bool(g_masks, cfg["K"]), g_s,
                   rules=cfg["prune"], cascade_k=(heur or {}).get("cascade_k", 0),
                   g_ph=g_ph if expl else None,
-                  g_win=g_win if ref else None, refine=ref)
+                  g_win=g_win if ref else None, refine=ref, g_gap=g_gap)
     chk.bind(ora)
     r_prev = None
     for t in range(T):

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert L.agft_abi_version() == L.ABI_VERSION == 4
+    assert L.agft_abi_version() == L.ABI_VERSION == 5
     for code in (0, -1, -2, -3, -4):
         assert L.agft_strerror(code)
     assert L.agft_strerror(-99) == "unknown status"
@@ -42,7 +42,7 @@ def test_abi_version_and_strerror(lib):
 
 def _cfg(**kw):
     base = dict(B=4, K=16, d=8, lambda_=1.0, alpha0=0.5, alpha_sched=0, prune_rule=0,
-                prune_period=50, flags=0)
+                prune_period=50, prune_sticky=1, flags=0)
     base.update(kw)
     return L.agft_config(**base)
 
@@ -77,6 +77,8 @@ def test_state_bytes(lib):
     for bad in (dict(B=0), dict(K=0), dict(K=1025), dict(lambda_=0.0), dict(lambda_=float("nan")),
                 dict(alpha0=-1.0), dict(alpha0=float("inf")), dict(alpha_sched=2),
                 dict(prune_rule=16), dict(prune_rule=-1), dict(prune_period=0), dict(flags=4), dict(d=12),
+                dict(prune_sticky=2), dict(prune_sticky=-1),
+                dict(prune_rule=3, prune_sticky=0, ext_rounds=60, ext_min_n=3, ext_thr=-1.2),
                 dict(prune_rule=2, ext_min_n=0), dict(prune_rule=2, ext_min_n=3, ext_thr=float("nan")),
                 dict(prune_rule=4, hist_min_n=0, hist_min_arms=3),
                 dict(prune_rule=4, hist_min_n=6, hist_min_arms=3, hist_kappa=-1.0),
@@ -110,6 +112,14 @@ def test_create_rejects_before_launch(lib):
     code, h = L.agft_create(cfg, ctypes.c_void_p(0x100000), n - 1, None)  # too small
     assert code == L.AGFT_E_INVAL
     code, h = L.agft_create(_cfg(d=12), ctypes.c_void_p(0x100000), 1 << 30, None)
+    assert code == L.AGFT_E_UNSUPPORTED
+    # a non-sticky rule 1 is built for rule 1 alone
+    heur = dict(ext_rounds=60, ext_min_n=3, ext_thr=-1.2)
+    code, h = L.agft_create(_cfg(prune_rule=3, prune_sticky=0, **heur), ctypes.c_void_p(0x100000),
+                            1 << 30, None)
+    assert code == L.AGFT_E_UNSUPPORTED
+    assert L.agft_state_bytes(_cfg(prune_rule=1, prune_sticky=0)) == n
+    code, shape = L.agft_launch_shape_for(_cfg(prune_rule=3, prune_sticky=0, **heur))
     assert code == L.AGFT_E_UNSUPPORTED
     code, h = L.agft_create(_cfg(alpha0=-1.0), ctypes.c_void_p(0x100000), 1 << 30, None)
     assert code == L.AGFT_E_INVAL

@@ -30,7 +30,8 @@ def _run_and_compare(wl, probes):
         f"{st['max_ctx_err']:.2e}, reward err {st['max_reward_err']:.2e}, forced "
         f"{st['forced']}/{st['decisions']}, prune forced {st['forced_prune']}, rules forced "
         f"{st['forced_rules']}, exact-tie steps "
-        f"{st['exact_tie_steps']}, theta err {wth:.2e}, Ainv err {wai:.2e}")
+        f"{st['exact_tie_steps']}, gap err {st['max_gap_err']:.2e}, theta err {wth:.2e}, "
+        f"Ainv err {wai:.2e}")
     return st
 
 

@@ -58,6 +58,10 @@ MUTANTS = {
     "greedy_scores_with_bonus": ("U[k] = greedy ? m : m + alpha * w;", "U[k] = m + alpha * w;"),
     "coarse_grid_from_bottom": ("return k >= lo && k <= hi && (hi - k) % st == 0;",
                                 "return k >= lo && k <= hi && (k - lo) % st == 0;"),
+    "nonsticky_ignores_action_space": ("                act0[k] = in_space(o, i, k);\n", "                act0[k] = 1;\n"),
+    "nonsticky_removals_stay": ("                kp[k] = 1;\n", "                kp[k] = glob[k];\n"),
+    "nonsticky_while_exploiting": ("if (prune_now && !o->sticky && !greedy)", "if (prune_now && !o->sticky)"),
+    "nonsticky_never": ("if (prune_now && !o->sticky && !greedy)", "if (0)"),
     "refine_min_samples_off_by_one": ("n[k] >= o->refine_min_n", "n[k] > o->refine_min_n"),
     "refine_anchor_worst_mean": ("rs[k] / n[k] > rs[anchor] / n[anchor]",
                                  "rs[k] / n[k] < rs[anchor] / n[anchor]"),
