@@ -6,7 +6,9 @@ A step is one decision for every instance of the workload: the tuner step
 kernel (pending update, scoring of every active arm, pruning, argmax) and the
 environment kernel that produces the next contexts and rewards.  All inputs
 (state, exogenous draws) are resident in HBM before the timed region, which
-times exactly K steps from a freshly initialised state.  Prints one JSON line.
+times exactly K steps from a freshly initialised state.  Then each of the five
+workloads is timed the same way over its whole horizon (detail.workloads).
+Prints one JSON line.
 """
 import argparse
 import hashlib
@@ -84,14 +86,17 @@ class TimingEvent:
             self._hip.hipEventDestroy(self._ev)
 
 
-def counter_traffic(workload, path=COUNTERS, source=STEP_SRC):
+def counter_traffic(workload, path=COUNTERS, source=STEP_SRC, steps=None, warmup=None):
     """HBM bytes per step-kernel launch from the committed counter summary,
-    or None unless it was taken on this workload with this kernel source."""
+    or None unless it was taken on this workload with this kernel source and
+    over the same window (timed steps after warm-up steps) as this run."""
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         cnt = json.load(fh)
     if cnt.get("source_sha256_16") != source_hash(source) or cnt.get("workload") != workload:
+        return None
+    if steps is not None and (cnt.get("steps"), cnt.get("warmup")) != (steps, warmup):
         return None
     return cnt.get("hbm_bytes_per_launch")
 
@@ -161,39 +166,23 @@ def cpu_baseline(wl, budget_s, threads=None, n_max=16384, max_steps=None):
                        f"environment, {el:.1f} s)", n=n, steps=steps)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's T)")
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="cfg4")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds for the oracle baseline")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--calibrate-copy", action="store_true",
-                    help="time the plain 1 GiB copy 3 times instead of 5 (for counter calibration runs)")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the tuner instances are independent, so a "
-              f"multi-GPU run is the same kernel on B/N instances per GPU (got --gpus {args.gpus})",
-              file=sys.stderr)
-        sys.exit(2)
-
+def measure(wl, K, W, dev, log_prefix="[bench]", draws=None):
+    """Run W untimed warm-up steps of workload wl, re-initialise, time K steps
+    from the fresh state (the step and environment kernels of each step),
+    replay them untimed to count the arms each step scored, and return the
+    figures of one bench line for this workload.  draws: the exogenous
+    arrays (arrivals, noise) of at least max(K, W) + 1 windows, if already made."""
     import numpy as np
     import torch
-    from agft_workloads import ENV, exogenous, get_workload
+    from agft_workloads import ENV, exogenous
     from paper_2508_01744_amd import GpuEnv, Tuner, env_config
 
-    wl = get_workload(args.workload)
-    K = wl.T if args.steps is None else args.steps
-    W = args.warmup
     T_env = max(K, W, 1)
-    dev = torch.device("cuda", 0)
-    torch.cuda.set_device(dev)
-    log(f"[bench] {wl.name}: B={wl.B} K={wl.K} d={wl.d}; timed steps {K}, warmup {W}")
-
-    arr, noi = exogenous(wl, T=T_env)
+    log(f"{log_prefix} {wl.name}: B={wl.B} K={wl.K} d={wl.d}; timed steps {K}, warmup {W}")
+    arr, noi = exogenous(wl, T=T_env) if draws is None else (draws[0][:T_env + 1], draws[1][:T_env + 1])
     arr_d = torch.as_tensor(arr, device=dev)
     noi_d = torch.as_tensor(noi, device=dev)
+    del arr, noi
     env = GpuEnv(env_config(wl, ENV, T=T_env), arr_d, noi_d)
     tuner = Tuner.from_workload(wl, device=dev)
     action = torch.empty(wl.B, dtype=torch.int32, device=dev)
@@ -258,22 +247,9 @@ def main():
     run(K, scored_log=scored_log)
     scored = torch.stack(scored_log).cpu().numpy().astype(np.int64) if scored_log else np.zeros((0, 4))
     torch.cuda.synchronize()
-
-    # a plain device copy (1 GiB read, 1 GiB written) as the bandwidth
-    # cross-check of the peak figure; its counter readings also calibrate
-    # the HBM counters (--calibrate-copy runs it under the profiler)
-    a = torch.empty(1 << 28, dtype=torch.float32, device=dev).normal_()
-    b = torch.empty_like(a)
-    torch.neg(a, out=b)
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 3 if args.calibrate_copy else 5
-    c0.record(stream)
-    for _ in range(reps):
-        torch.neg(a, out=b)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    copy_gbs = reps * 2 * a.numel() * 4 / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    del a, b
+    tuner.close()
+    del tuner, env, arr_d, noi_d
+    torch.cuda.empty_cache()
 
     total_bytes = 0.0
     for t in range(K):
@@ -282,18 +258,96 @@ def main():
     bytes_per_launch = total_bytes / K
     kernel_avg_ms = float(kernel_ms.mean())
     achieved = bytes_per_launch / (kernel_avg_ms * 1e-3) / 1e9
+    return dict(value=wl.B * K / (elapsed_ms * 1e-3), ms_per_step=elapsed_ms / K, steps=K,
+                step_kernel_avg_ms=kernel_avg_ms,
+                step_kernel_median_ms=float(np.median(kernel_ms)),
+                step_kernel_share=float(kernel_ms.sum() / elapsed_ms),
+                algorithmic_bytes_per_launch=bytes_per_launch,
+                achieved_gbs=achieved, frac=achieved / HBM_PEAK_GBS,
+                mean_scored_arms=float(scored[:, :2].sum(axis=1).mean() / wl.B) if K else None,
+                mean_active_arms_after_step=float(scored[:, 2].mean() / wl.B) if K else None,
+                exploiting_fraction=float(scored[:, 3].mean() / wl.B) if K else None,
+                wall_s=t_wall)
 
-    traffic = counter_traffic(wl.name)
 
-    value = wl.B * K / (elapsed_ms * 1e-3)
+def byte_model(wl):
+    """What the algorithmic byte count charges per arm, against the dense
+    d x d inverse-plus-vector layout a plain implementation of Eq. 1-5 keeps."""
+    d = wl.d
+    return {"layout": "packed: theta and the upper-triangular factor S (S S^T = A^-1) of each arm",
+            "model_bytes_per_arm": 4 * record_floats(d),
+            "dense_bytes_per_arm": 4 * (d * d + d),
+            "counted": "every scored arm's model read once (theta alone for an exploiting instance), "
+                       "the updated arm read and written, the per-instance words and mask"}
+
+
+def copy_rate(dev, reps):
+    """A plain device copy (1 GiB read, 1 GiB written) as the bandwidth
+    cross-check of the peak figure; its counter readings also calibrate the
+    HBM counters (--calibrate-copy runs it under the profiler)."""
+    import torch
+    stream = torch.cuda.current_stream(dev)
+    a = torch.empty(1 << 28, dtype=torch.float32, device=dev).normal_()
+    b = torch.empty_like(a)
+    torch.neg(a, out=b)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(reps):
+        torch.neg(a, out=b)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    gbs = reps * 2 * a.numel() * 4 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del a, b
+    torch.cuda.empty_cache()
+    return gbs
+
+
+# the other workloads, timed over their whole horizon beside the headline
+DETAIL_WORKLOADS = ("cfg1", "cfg2", "cfg3", "cfg4", "cfg5")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's T)")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="cfg4")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds for the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the runs of the other workloads reported under detail.workloads")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="time the plain 1 GiB copy 3 times instead of 5 (for counter calibration runs)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the tuner instances are independent, so a "
+              f"multi-GPU run is the same kernel on B/N instances per GPU (got --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from agft_workloads import get_workload
+
+    wl = get_workload(args.workload)
+    K = wl.T if args.steps is None else args.steps
+    W = args.warmup
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    # the headline's draws serve its own run over the whole horizon too
+    from agft_workloads import exogenous
+    draws = exogenous(wl, T=max(K, W, wl.T if wl.name in DETAIL_WORKLOADS else 1, 1))
+    head = measure(wl, K, W, dev, draws=draws)
+    copy_gbs = copy_rate(dev, 3 if args.calibrate_copy else 5)
+    traffic = counter_traffic(wl.name, steps=K, warmup=W)
+
     res = {
         "metric": "bandit decision-steps/sec (instances x steps) + achieved HBM GB/s vs peak",
-        "value": value,
+        "value": head["value"],
         "unit": "decision-steps/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": W,
-        "ms_per_step": elapsed_ms / K,
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -301,17 +355,34 @@ def main():
         "data": "synthetic (seeded load traces, closed-form energy-delay reward)",
         "config": {"workload": f"{wl.name}: {wl.description}", "instances": wl.B, "arms": wl.K,
                    "context_dim": wl.d, "steps_per_run": wl.T, "parallelism": "none (1 GPU)"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
-        "detail": {"step_kernel_avg_ms": kernel_avg_ms,
-                   "step_kernel_share": float(kernel_ms.sum() / elapsed_ms),
-                   "algorithmic_bytes_per_launch": bytes_per_launch,
-                   "mean_scored_arms": float(scored[:, :2].sum(axis=1).mean() / wl.B) if K else None,
-                   "mean_active_arms_after_step": float(scored[:, 2].mean() / wl.B) if K else None,
-                   "exploiting_fraction": float(scored[:, 3].mean() / wl.B) if K else None,
-                   "device_copy_gbs": copy_gbs,
-                   "wall_s": t_wall},
+        "roofline": {"bound": "hbm", "achieved": head["achieved_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": head["frac"], "traffic": traffic,
+                     "traffic_window": (f"HBM bytes per step-kernel launch over the same {K} timed steps "
+                                        f"(after {W} warm-up steps) of {wl.name}, from rocprofv3 counters "
+                                        f"on this kernel source" if traffic is not None else None),
+                     "byte_model": byte_model(wl)},
+        "detail": {k: head[k] for k in ("step_kernel_avg_ms", "step_kernel_median_ms", "step_kernel_share",
+                                        "algorithmic_bytes_per_launch", "mean_scored_arms",
+                                        "mean_active_arms_after_step", "exploiting_fraction", "wall_s")},
     }
+    res["detail"]["device_copy_gbs"] = copy_gbs
+    if not args.no_workloads:
+        runs = {}
+        for name in DETAIL_WORKLOADS:
+            if name == wl.name and args.steps is None:
+                runs[name] = head
+                continue
+            w2 = get_workload(name)
+            runs[name] = measure(w2, w2.T, W, dev, log_prefix="[bench detail]",
+                                 draws=draws if name == wl.name else None)
+        res["detail"]["workloads"] = {
+            name: {"steps": r["steps"], "decision_steps_per_s": r["value"], "ms_per_step": r["ms_per_step"],
+                   "step_kernel_avg_ms": r["step_kernel_avg_ms"], "achieved_gbs": r["achieved_gbs"],
+                   "frac": r["frac"], "mean_scored_arms": r["mean_scored_arms"]}
+            for name, r in runs.items()}
+        res["detail"]["workloads_note"] = ("each workload timed over its whole horizon from a fresh state, "
+                                           "step and environment kernels, inputs resident; frac = algorithmic "
+                                           "bytes per step-kernel launch over its average duration, of 8 TB/s")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
         base = cpu_baseline(wl, args.cpu_budget)

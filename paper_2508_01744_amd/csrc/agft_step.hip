@@ -557,6 +557,7 @@ void agft_step_kernel(StepArgs p) {
 
     __shared__ float s_xp[D];   // context of the previous decision, for the update
     __shared__ int2 s_stu;      // its arm's reward count and sum
+    __shared__ int2 s_cmap[R::R];   // canonical indices of its record's chunks, for the write-back
 
     const bool decide = p.ctx != nullptr;
     // the instance's mask words, issued first: they depend on nothing, and the
@@ -801,6 +802,7 @@ void agft_step_kernel(StepArgs p) {
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
             if (c < R::R) {
+                s_cmap[c] = cmap[q];
                 const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
@@ -836,8 +838,9 @@ void agft_step_kernel(StepArgs p) {
 
     // ---- square-root rank-1 update of the previous decision's arm ----
     // Run while the stream's first pass is in flight, or after the stream
-    // (early_update on the host decides which).
-    auto update = [&](const int2 *cm) {
+    // (early_update on the host decides which), in LDS; the updated record
+    // is written back as the kernel's last act (write_back below).
+    auto update = [&]() {
         if (upd) {
             const float *sth = s_old;         // theta
             const float *sS = s_old + D;      // packed factor
@@ -888,15 +891,28 @@ void agft_step_kernel(StepArgs p) {
                 if (i < D && jc == D - 1) s_new[i] = fmaf(qi / al_last, err, sth[i]);
             }
             __syncthreads();
+        } else if (has_prev && tid == 0) {
+            blk[kInstBad] += 1;
+        }
+    };
+    // The updated record, its theta copy and its reward count and sum go out
+    // last.  Loads and stores share one completion counter on this
+    // architecture, and the compiler's waits for the stream's loads do not
+    // follow paths: a store issued before a wait for a load is waited for too,
+    // so stores in the middle of the step would hold up the rest of it by
+    // their full latency.
+    auto write_back = [&]() {
+        if (upd) {
             float4 *dst = p.arms + (size_t)inst * inst_chunks;
 #pragma unroll
             for (int q = 0; q < NQ; ++q) {
                 const int c = tid + q * nthr;
                 if (c < R::R) {
+                    const int2 cm = s_cmap[c];
                     float v[4];
 #pragma unroll
                     for (int qq = 0; qq < 4; ++qq) {
-                        const int ci = map_at(cm[q], qq);
+                        const int ci = map_at(cm, qq);
                         v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
                     }
                     st_record<D>(dst + rec_chunk(D, TF, a_upd, c), v[0], v[1], v[2], v[3]);
@@ -909,14 +925,12 @@ void agft_step_kernel(StepArgs p) {
             if (p.keep_stats && tid == 0)
                 p.stats[(size_t)inst * K + a_upd] =
                     make_int2(s_stu.x + 1, __float_as_int(__int_as_float(s_stu.y) + r));
-        } else if (has_prev && tid == 0) {
-            blk[kInstBad] += 1;
         }
     };
     // An exploiting instance has no pass in flight.  Where the whole list fits
     // in the first pass, no later pass can wait behind the update.
     const bool early = (p.early_update || nlist <= apw) && !greedy;
-    if (early) update(cmap);
+    if (early) update();
 
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
     if (greedy) {
@@ -990,17 +1004,7 @@ void agft_step_kernel(StepArgs p) {
         }
     }
 
-    if (!early) {
-        // the chunk map again (registers held through the stream would cost
-        // occupancy); its load overlaps the update's first phase
-        int2 cml[NQ];
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-            const int c = tid + q * nthr;
-            cml[q] = upd && c < R::R ? ld_chunk_map<D, TF>(c) : make_int2(0, 0);
-        }
-        update(cml);
-    }
+    if (!early) update();
 
     // the updated arm, scored on x_t from LDS in the streaming order
     if (upd && x_ok && wave == 0) {
@@ -1028,6 +1032,7 @@ void agft_step_kernel(StepArgs p) {
             if (inst == 0) p.hdr->pending = 0;
         }
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
+        write_back();
         return;
     }
 
@@ -1049,6 +1054,7 @@ void agft_step_kernel(StepArgs p) {
             }
         }
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
+        write_back();
         return;
     }
     __syncthreads();
@@ -1087,8 +1093,10 @@ void agft_step_kernel(StepArgs p) {
             }
             if (stat_anchor) {
                 // best mean reward among the arms with enough rewards (this
-                // step's update already counted)
-                const int2 v = p.stats[(size_t)inst * K + k];
+                // step's update already counted: the updated arm's count and
+                // sum are written back only at the end of the step)
+                const int2 v = k == a_upd ? make_int2(s_stu.x + 1, __float_as_int(__int_as_float(s_stu.y) + r))
+                                          : p.stats[(size_t)inst * K + k];
                 if (v.x >= p.rf.min_n) sb = better(sb, BestPair{__int_as_float(v.y) / (float)v.x, k});
             }
         }
@@ -1198,6 +1206,7 @@ void agft_step_kernel(StepArgs p) {
         if (lane >= kInstX && lane < kInstX + D)
             reinterpret_cast<float *>(blk)[lane] = pick<D>(x, lane - kInstX);
     }
+    write_back();
 }
 
 // ---- initialisation and export ----

@@ -54,6 +54,12 @@ def test_traffic_only_for_the_profiled_source_and_workload(tmp_path):
     write()
     assert bench.counter_traffic("cfg4", str(path), str(src)) == 5.1e9
     assert bench.counter_traffic("cfg3", str(path), str(src)) is None
+    # counters taken over another window of steps are not this run's traffic
+    write(steps=20, warmup=5)
+    assert bench.counter_traffic("cfg4", str(path), str(src), steps=20, warmup=5) == 5.1e9
+    assert bench.counter_traffic("cfg4", str(path), str(src), steps=500, warmup=5) is None
+    assert bench.counter_traffic("cfg4", str(path), str(src), steps=20, warmup=20) is None
+    write()
     src.write_text("kernel source, changed\n")
     assert bench.counter_traffic("cfg4", str(path), str(src)) is None
     assert bench.counter_traffic("cfg4", str(tmp_path / "absent.json"), str(src)) is None
@@ -68,3 +74,10 @@ def test_oracle_baselines():
     assert one["cores"] == 1 and one["n"] == 8 and one["steps"] == 10
     # the thread count is restored afterwards
     assert bench.cpu_baseline(wl, 5.0, max_steps=1)["cores"] == allc["cores"]
+
+
+def test_byte_model_states_both_layouts():
+    bm = bench.byte_model(get_workload("cfg4"))
+    assert bm["model_bytes_per_arm"] == 608 and bm["dense_bytes_per_arm"] == 1088
+    bm = bench.byte_model(get_workload("cfg5"))
+    assert bm["model_bytes_per_arm"] == 4 * (32 + 528) and bm["dense_bytes_per_arm"] == 4 * (1024 + 32)

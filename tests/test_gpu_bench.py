@@ -16,7 +16,7 @@ def test_bench_json_line():
     cmd = [sys.executable, "-u", os.path.join(ROOT, "bench.py"), "--workload", "cfg2", "--steps", "30",
            "--warmup", "3", "--cpu-budget", "1"]
     print("[bench test]", " ".join(cmd[2:]), flush=True)
-    r = subprocess.run(cmd, capture_output=True, text=True, timeout=240, cwd=ROOT)
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=280, cwd=ROOT)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [l for l in r.stdout.splitlines() if l.strip()]
     assert len(lines) == 1, r.stdout
@@ -42,3 +42,11 @@ def test_bench_json_line():
     assert cb["kind"] == "oracle" and cb["unit"] == "decision-steps/s" and cb["value"] > 0
     assert cb["cores"] >= 1 and "cfg2" in cb["sample"]
     assert det["cpu_oracle_1thread"]["cores"] == 1
+    assert rf["byte_model"]["model_bytes_per_arm"] == 176 and rf["byte_model"]["dense_bytes_per_arm"] == 288
+    # every workload over its whole horizon beside the headline
+    wls = det["workloads"]
+    assert set(wls) == {"cfg1", "cfg2", "cfg3", "cfg4", "cfg5"}
+    for name, w in wls.items():
+        steps = {"cfg1": 10000, "cfg2": 2000, "cfg3": 1000, "cfg4": 500, "cfg5": 2000}[name]
+        assert w["steps"] == steps and w["decision_steps_per_s"] > 0 and 0 < w["frac"] < 1.5
+        assert 0 < w["step_kernel_avg_ms"] < w["ms_per_step"] and w["mean_scored_arms"] > 0
