@@ -141,32 +141,43 @@ __host__ __device__ constexpr int canon_chunk(int D, int TF, int c, int q) {
     return t % TF < 3 ? canon(D, t / TF, D + t % TF) : -1;
 }
 
-// Canonical indices of the four components of every record chunk (-1 for
-// padding), built at compile time and read from constant memory, one 8-byte
-// load per chunk, instead of being recomputed by each thread.
+// Float offset, within an arm's record (chunks in record order), of factor
+// element S_ij (i <= j) and of theta_i: column j < G sits in lane slice j at
+// position i, column j >= G in slice D-1-j at position D-i; theta_i at
+// position D+1+(i%2) of slice i/2.  Positions below D are component e%4 of
+// main chunk (e/4)*G + slice, the others tail float TF*slice + (e-D).
 template <int D, int TF>
-struct ChunkMap {
-    int16_t ci[(D / 2) * (D / 4) + (D / 2) * TF / 4][4];
-};
-template <int D, int TF>
-constexpr ChunkMap<D, TF> make_chunk_map() {
-    ChunkMap<D, TF> m{};
-    for (int c = 0; c < (D / 2) * (D / 4) + (D / 2) * TF / 4; ++c)
-        for (int q = 0; q < 4; ++q) m.ci[c][q] = (int16_t)canon_chunk(D, TF, c, q);
-    return m;
+__host__ __device__ constexpr int rec_pos_S(int i, int jc) {
+    constexpr int G = D / 2, MAIN = G * (D / 4);
+    const bool first = jc < G;
+    const int sl = first ? jc : D - 1 - jc;
+    const int e = first ? i : D - i;
+    return e < D ? 4 * ((e >> 2) * G + sl) + (e & 3) : 4 * MAIN + TF * sl + (e - D);
 }
 template <int D, int TF>
-__constant__ ChunkMap<D, TF> kChunkMap = make_chunk_map<D, TF>();
+__host__ __device__ constexpr int rec_pos_theta(int i) {
+    constexpr int G = D / 2, MAIN = G * (D / 4);
+    return 4 * MAIN + TF * (i >> 1) + 1 + (i & 1);
+}
 
+// The two offset functions above invert canon_chunk: checked at compile time
+// for every record layout the kernels are built for.
 template <int D, int TF>
-__device__ __forceinline__ int2 ld_chunk_map(int c) {
-    return *reinterpret_cast<const int2 *>(&kChunkMap<D, TF>.ci[c][0]);
+constexpr bool rec_pos_consistent() {
+    for (int jc = 0; jc < D; ++jc)
+        for (int i = 0; i <= jc; ++i) {
+            const int pos = rec_pos_S<D, TF>(i, jc);
+            if (canon_chunk(D, TF, pos / 4, pos % 4) != D + packed(i, jc)) return false;
+        }
+    for (int i = 0; i < D; ++i) {
+        const int pos = rec_pos_theta<D, TF>(i);
+        if (canon_chunk(D, TF, pos / 4, pos % 4) != i) return false;
+    }
+    return true;
 }
-// component q of a chunk's map entry
-__device__ __forceinline__ int map_at(int2 m, int q) {
-    const int w = q < 2 ? m.x : m.y;
-    return (q & 1) ? (w >> 16) : (int)(int16_t)(w & 0xffff);
-}
+static_assert(rec_pos_consistent<8, 3>() && rec_pos_consistent<8, 4>() && rec_pos_consistent<16, 3>() &&
+                  rec_pos_consistent<16, 4>() && rec_pos_consistent<32, 3>() && rec_pos_consistent<32, 4>(),
+              "record offsets of the update disagree with the record layout");
 
 // Column j and row i of packed element e.
 __device__ inline void unpack(int e, int &i, int &j) {
@@ -536,8 +547,12 @@ void agft_step_kernel(StepArgs p) {
     const size_t inst_chunks = (size_t)((K + R::NB - 1) / R::NB) * R::BLK;
     const float4 *recs = p.arms + (size_t)inst * inst_chunks;
 
-    __shared__ float s_old[R::CAN];
-    __shared__ float s_new[R::CAN];
+    // the previous decision's record before and after its update, chunks in
+    // record order (the layout of the arm's record in HBM)
+    __shared__ float4 s_old4[R::R];
+    __shared__ float4 s_new4[R::R];
+    float *s_old = reinterpret_cast<float *>(s_old4);
+    float *s_new = reinterpret_cast<float *>(s_new4);
     __shared__ float s_fpart[NW][D];   // per-wavefront partial sums of f = S^T xp
     // per-arm scores and the list of arms to stream, sized by K at launch
     // (step_lds_bytes) so that small arm counts leave room for more workgroups
@@ -557,7 +572,6 @@ void agft_step_kernel(StepArgs p) {
 
     __shared__ float s_xp[D];   // context of the previous decision, for the update
     __shared__ int2 s_stu;      // its arm's reward count and sum
-    __shared__ int2 s_cmap[R::R];   // canonical indices of its record's chunks, for the write-back
 
     const bool decide = p.ctx != nullptr;
     // the instance's mask words, issued first: they depend on nothing, and the
@@ -572,15 +586,32 @@ void agft_step_kernel(StepArgs p) {
     bool x_ok = decide;
     if (decide) {
         const float *xi = p.ctx + (size_t)inst * D;
+        // non-finite test on the exponent bits, in scalar integer arithmetic
+        uint32_t nonfinite = 0u;
 #pragma unroll
         for (int q = 0; q < D; ++q) {
             x[q] = xi[q];
-            x_ok = x_ok && isfinite(x[q]);
+            nonfinite |= (__float_as_uint(x[q]) & 0x7f800000u) == 0x7f800000u ? 1u : 0u;
         }
+        x_ok = nonfinite == 0u;
     } else {
 #pragma unroll
         for (int q = 0; q < D; ++q) x[q] = 0.0f;
     }
+    // The context also waits in LDS for its later readers (the exploiting
+    // stream and the stash in the epilogue), so that its D scalar registers
+    // die once this lane's selectors below are formed: held through the step
+    // at D = 32 they would push the scalar registers into spills.
+    __shared__ float s_x[D];
+    if (wave == 0 && lane < D) s_x[lane] = decide ? p.ctx[(size_t)inst * D + lane] : 0.0f;
+    // This lane's selectors of x: xa_e = x_e for e <= j, xb_e = x_{D-e} for e > j.
+    float xa[D + 1], xb[D + 1];
+#pragma unroll
+    for (int e = 0; e <= D; ++e) {
+        xa[e] = e <= j ? x[e] : 0.0f;
+        xb[e] = (e > j && e >= 1) ? x[D - e < 0 ? 0 : D - e] : 0.0f;
+    }
+    const float xt0 = pick<D>(x, 2 * j), xt1 = pick<D>(x, 2 * j + 1);
     int32_t *blk = p.inst + (size_t)inst * p.IW;
     const int a_prev = p.apply_update ? blk[kInstAprev] : -1;
     const bool has_prev = a_prev >= 0 && a_prev < K;
@@ -634,17 +665,12 @@ void agft_step_kernel(StepArgs p) {
     // they would wait behind the record's write-back (stores and loads share
     // one completion counter), about 6 us per workgroup.
     float4 old_chunk[NQ];
-    int2 cmap[NQ];   // canonical indices of those chunks
     int2 st_upd = make_int2(0, 0);
     if (upd) {
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
-            cmap[q] = make_int2(0, 0);
-            if (c < R::R) {
-                old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
-                cmap[q] = ld_chunk_map<D, TF>(c);
-            }
+            if (c < R::R) old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
         }
         if (p.keep_stats && tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
     }
@@ -786,30 +812,14 @@ void agft_step_kernel(StepArgs p) {
         if (lane == 0) s_nlist = placed;
     }
 
-    // This lane's selectors of x: xa_e = x_e for e <= j, xb_e = x_{D-e} for e > j.
-    float xa[D + 1], xb[D + 1];
-#pragma unroll
-    for (int e = 0; e <= D; ++e) {
-        xa[e] = e <= j ? x[e] : 0.0f;
-        xb[e] = (e > j && e >= 1) ? x[D - e < 0 ? 0 : D - e] : 0.0f;
-    }
-    const float xt0 = pick<D>(x, 2 * j), xt1 = pick<D>(x, 2 * j + 1);
-    // The previous decision's record, fetched at kernel start, goes to LDS in
-    // canonical order now, so that it holds no registers through the stream.
+    // The previous decision's record, fetched at kernel start, goes to LDS now,
+    // so that it holds no registers through the stream.
     if (upd) {
         if (tid == 0) s_stu = st_upd;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
             const int c = tid + q * nthr;
-            if (c < R::R) {
-                s_cmap[c] = cmap[q];
-                const float v[4] = {old_chunk[q].x, old_chunk[q].y, old_chunk[q].z, old_chunk[q].w};
-#pragma unroll
-                for (int qq = 0; qq < 4; ++qq) {
-                    const int ci = map_at(cmap[q], qq);
-                    if (ci >= 0) s_old[ci] = v[qq];
-                }
-            }
+            if (c < R::R) s_old4[c] = old_chunk[q];
         }
     }
     __syncthreads();
@@ -842,8 +852,6 @@ void agft_step_kernel(StepArgs p) {
     // is written back as the kernel's last act (write_back below).
     auto update = [&]() {
         if (upd) {
-            const float *sth = s_old;         // theta
-            const float *sS = s_old + D;      // packed factor
             // Lane l of every wavefront takes column j = l % D of one row per
             // pass (row segments of D lanes; a pass of the workgroup covers RP
             // rows), so that the column sums and the row prefix sums below are
@@ -856,7 +864,7 @@ void agft_step_kernel(StepArgs p) {
 #pragma unroll
             for (int ps = 0; ps < NP; ++ps) {
                 const int i = ps * RP + wave * SEGS + seg;
-                if (i < D && i <= jc) fj = fmaf(sS[packed(i, jc)], s_xp[i], fj);
+                if (i < D && i <= jc) fj = fmaf(s_old[rec_pos_S<D, TF>(i, jc)], s_xp[i], fj);
             }
             fj = segment_colsum<D>(fj);
             if constexpr (NW > 1) {
@@ -874,7 +882,7 @@ void agft_step_kernel(StepArgs p) {
             const float ca = sqrtf(al_prev / al), cb = fj / sqrtf(al_prev * al);
             const float al_last = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(al), D - 1));
             // prediction error r - xp^T theta
-            float pred = lane < D ? s_xp[lane] * sth[lane] : 0.0f;
+            float pred = lane < D ? s_xp[lane] * s_old[rec_pos_theta<D, TF>(lane)] : 0.0f;
             pred = wave_reduce(pred, [](float a, float b) { return a + b; });
             const float err = r - pred;
             // row i of S' = S M:  S'_ij = ca_j S_ij - cb_j g_ij with g_ij the
@@ -884,12 +892,19 @@ void agft_step_kernel(StepArgs p) {
             for (int ps = 0; ps < NP; ++ps) {
                 const int i = ps * RP + wave * SEGS + seg;
                 const bool in_row = i < D && i <= jc;
-                const float sij = in_row ? sS[packed(i, jc)] : 0.0f;
+                const int pos = rec_pos_S<D, TF>(i < D ? i : 0, jc);
+                const float sij = in_row ? s_old[pos] : 0.0f;
                 const float q = fj * sij;
                 const float qi = segment_scan<D>(q, lane);
-                if (in_row) s_new[D + packed(i, jc)] = ca * sij - cb * (qi - q);
-                if (i < D && jc == D - 1) s_new[i] = fmaf(qi / al_last, err, sth[i]);
+                if (in_row) s_new[pos] = ca * sij - cb * (qi - q);
+                if (i < D && jc == D - 1) {
+                    const int tp = rec_pos_theta<D, TF>(i);
+                    s_new[tp] = fmaf(qi / al_last, err, s_old[tp]);
+                }
             }
+            // padded tails: the fourth float of each lane slice's tail stays 0
+            if constexpr (TF == 4)
+                if (tid < G) s_new[4 * R::MAIN + 4 * tid + 3] = 0.0f;
             __syncthreads();
         } else if (has_prev && tid == 0) {
             blk[kInstBad] += 1;
@@ -908,19 +923,14 @@ void agft_step_kernel(StepArgs p) {
             for (int q = 0; q < NQ; ++q) {
                 const int c = tid + q * nthr;
                 if (c < R::R) {
-                    const int2 cm = s_cmap[c];
-                    float v[4];
-#pragma unroll
-                    for (int qq = 0; qq < 4; ++qq) {
-                        const int ci = map_at(cm, qq);
-                        v[qq] = ci >= 0 ? s_new[ci] : 0.0f;
-                    }
-                    st_record<D>(dst + rec_chunk(D, TF, a_upd, c), v[0], v[1], v[2], v[3]);
+                    const float4 v = s_new4[c];
+                    st_record<D>(dst + rec_chunk(D, TF, a_upd, c), v.x, v.y, v.z, v.w);
                 }
             }
             if (p.theta != nullptr && tid < D / 4) {
                 float4 *tdst = reinterpret_cast<float4 *>(p.theta + ((size_t)inst * K + a_upd) * D);
-                tdst[tid] = make_float4(s_new[4 * tid], s_new[4 * tid + 1], s_new[4 * tid + 2], s_new[4 * tid + 3]);
+                tdst[tid] = make_float4(s_new[rec_pos_theta<D, TF>(4 * tid)], s_new[rec_pos_theta<D, TF>(4 * tid + 1)],
+                                        s_new[rec_pos_theta<D, TF>(4 * tid + 2)], s_new[rec_pos_theta<D, TF>(4 * tid + 3)]);
             }
             if (p.keep_stats && tid == 0)
                 p.stats[(size_t)inst * K + a_upd] =
@@ -938,8 +948,8 @@ void agft_step_kernel(StepArgs p) {
         // groups of D/4 lanes (one float4 each)
         constexpr int GT = D / 4;
         const int jt = tid % GT, gt = tid / GT, apt = nthr / GT;
-        const float x0 = pick<D>(x, 4 * jt), x1 = pick<D>(x, 4 * jt + 1);
-        const float x2 = pick<D>(x, 4 * jt + 2), x3 = pick<D>(x, 4 * jt + 3);
+        const float x0 = s_x[4 * jt], x1 = s_x[4 * jt + 1];
+        const float x2 = s_x[4 * jt + 2], x3 = s_x[4 * jt + 3];
         const float4 *th = reinterpret_cast<const float4 *>(p.theta + (size_t)inst * K * D);
         // UT passes' loads are issued before any of them is used, so that an
         // instance waits for about one load latency per UT passes (three at
@@ -1006,14 +1016,23 @@ void agft_step_kernel(StepArgs p) {
 
     if (!early) update();
 
-    // the updated arm, scored on x_t from LDS in the streaming order
+    // the updated arm, scored on x_t from LDS exactly as the stream scores a
+    // record from HBM (same slices, same operation order)
     if (upd && x_ok && wave == 0) {
         float f[4 * S];
 #pragma unroll
-        for (int e = 0; e < 4 * S; ++e) {
-            const int ci = canon(D, j, e);
-            f[e] = ci >= 0 ? s_new[ci] : 0.0f;
+        for (int sidx = 0; sidx < R::MQ; ++sidx) {
+            const float4 c4 = s_new4[sidx * G + j];
+            f[4 * sidx] = c4.x;
+            f[4 * sidx + 1] = c4.y;
+            f[4 * sidx + 2] = c4.z;
+            f[4 * sidx + 3] = c4.w;
         }
+        const float *tl = s_new + 4 * R::MAIN + TF * j;
+        f[4 * R::MQ] = tl[0];
+        f[4 * R::MQ + 1] = tl[1];
+        f[4 * R::MQ + 2] = tl[2];
+        f[4 * R::MQ + 3] = 0.0f;
         float m, w2;
         slice_terms<D>(f, xa, xb, xt0, xt1, m, w2);
         m = group_sum<G>(m);
@@ -1204,7 +1223,7 @@ void agft_step_kernel(StepArgs p) {
             blk[lane] = lane == kInstLo ? nlo : (lane == kInstHi ? nhi : 1);
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
         if (lane >= kInstX && lane < kInstX + D)
-            reinterpret_cast<float *>(blk)[lane] = pick<D>(x, lane - kInstX);
+            reinterpret_cast<float *>(blk)[lane] = s_x[lane - kInstX];
     }
     write_back();
 }
