@@ -241,6 +241,19 @@ def measure(wl, K, W, dev, log_prefix="[bench]", draws=None):
     elapsed_ms = start.elapsed_time(stop)
     kernel_ms = np.array([a.elapsed_time(b) for a, b in ev])
 
+    # the same steps with the decision and the environment's response fused
+    # into one launch per step (agft_sim_step)
+    fresh()
+    torch.cuda.synchronize()
+    f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    env.reset()
+    f0.record(stream)
+    for t in range(K):
+        env.fused_step(tuner, action)
+    f1.record(stream)
+    torch.cuda.synchronize()
+    fused_ms = f0.elapsed_time(f1)
+
     # the run is deterministic: replay it untimed to log the arms each step scored
     fresh()
     scored_log = []
@@ -259,6 +272,7 @@ def measure(wl, K, W, dev, log_prefix="[bench]", draws=None):
     kernel_avg_ms = float(kernel_ms.mean())
     achieved = bytes_per_launch / (kernel_avg_ms * 1e-3) / 1e9
     return dict(value=wl.B * K / (elapsed_ms * 1e-3), ms_per_step=elapsed_ms / K, steps=K,
+                value_fused=wl.B * K / (fused_ms * 1e-3), ms_per_step_fused=fused_ms / K,
                 step_kernel_avg_ms=kernel_avg_ms,
                 step_kernel_median_ms=float(np.median(kernel_ms)),
                 step_kernel_share=float(kernel_ms.sum() / elapsed_ms),
@@ -362,6 +376,7 @@ def main():
                                         f"on this kernel source" if traffic is not None else None),
                      "byte_model": byte_model(wl)},
         "detail": {k: head[k] for k in ("step_kernel_avg_ms", "step_kernel_median_ms", "step_kernel_share",
+                                        "ms_per_step_fused",
                                         "algorithmic_bytes_per_launch", "mean_scored_arms",
                                         "mean_active_arms_after_step", "exploiting_fraction", "wall_s")},
     }
@@ -377,12 +392,15 @@ def main():
                                  draws=draws if name == wl.name else None)
         res["detail"]["workloads"] = {
             name: {"steps": r["steps"], "decision_steps_per_s": r["value"], "ms_per_step": r["ms_per_step"],
+                   "decision_steps_per_s_fused": r["value_fused"], "ms_per_step_fused": r["ms_per_step_fused"],
                    "step_kernel_avg_ms": r["step_kernel_avg_ms"], "achieved_gbs": r["achieved_gbs"],
                    "frac": r["frac"], "mean_scored_arms": r["mean_scored_arms"]}
             for name, r in runs.items()}
         res["detail"]["workloads_note"] = ("each workload timed over its whole horizon from a fresh state, "
-                                           "step and environment kernels, inputs resident; frac = algorithmic "
-                                           "bytes per step-kernel launch over its average duration, of 8 TB/s")
+                                           "step and environment kernels, inputs resident; *_fused: the same "
+                                           "steps with the environment in the step kernel's epilogue "
+                                           "(agft_sim_step, one launch per step); frac = algorithmic bytes per "
+                                           "step-kernel launch over its average duration, of 8 TB/s")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
         base = cpu_baseline(wl, args.cpu_budget)

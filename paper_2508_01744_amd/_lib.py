@@ -59,7 +59,7 @@ ABI_VERSION = 5   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
             "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version", "agft_launch_shape_for",
-            "agft_env_state_bytes", "agft_env_reset", "agft_env_step"]
+            "agft_env_state_bytes", "agft_env_reset", "agft_env_step", "agft_sim_step"]
 
 _lib = None
 
@@ -100,6 +100,8 @@ def _declare(lib):
     lib.agft_env_reset.argtypes = [envp, _vp, _sz, _vp, _vp, _vp, _vp]
     lib.agft_env_step.restype = ctypes.c_int
     lib.agft_env_step.argtypes = [envp, _vp, _sz, _i32, _vp, _vp, _vp, _vp, _vp, _vp]
+    lib.agft_sim_step.restype = ctypes.c_int
+    lib.agft_sim_step.argtypes = [_vp, envp, _vp, _sz, _vp, _vp, _vp, _vp, _vp, _vp]
     return lib
 
 
@@ -183,3 +185,8 @@ def agft_env_reset(cfg, d_env, nbytes, d_arrivals, d_noise, d_ctx, stream):
 def agft_env_step(cfg, d_env, nbytes, t, d_action, d_arrivals, d_noise, d_reward, d_ctx, stream):
     return lib().agft_env_step(ctypes.byref(cfg), d_env, nbytes, t, d_action, d_arrivals, d_noise,
                                d_reward, d_ctx, stream)
+
+
+def agft_sim_step(h, env_cfg, d_env, env_nbytes, d_arrivals, d_noise, d_ctx, d_reward, d_action, d_scores):
+    return lib().agft_sim_step(h, ctypes.byref(env_cfg), d_env, env_nbytes, d_arrivals, d_noise, d_ctx,
+                               d_reward, d_action, d_scores)

@@ -51,6 +51,7 @@
 #include <type_traits>
 
 #include "agft.h"
+#include "agft_env_math.h"
 
 namespace {
 
@@ -527,9 +528,15 @@ int occupancy_for(const agft_config &c, int tail) {
     return c.d == 16 && tail == 3 && !(c.prune_rule & 14) ? 6 : 7;
 }
 
-template <int D, int TF, int W, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(W)))
-void agft_step_kernel(StepArgs p) {
+// ENV: the simulator's environment responds in the epilogue (agft_sim_step):
+// once the decision is known, the first lanes of wavefront 0 run the
+// instance's next window with it, writing the reward and the next context in
+// place of the ones read.  The word each of those lanes prefetches costs a
+// register: at d = 16 the seven-wavefront form gets six, to fit without
+// spilling.
+template <int D, int TF, int W, int NW, bool ENV>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(ENV && D == 16 && W > 6 ? W - 1 : W)))
+void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
     using R = Rec<D, TF>;
     constexpr int G = R::G, S = R::S;
     constexpr int NQ = (R::R + kWave - 1) / kWave;   // update-record chunks per thread (>= 64 threads)
@@ -604,6 +611,11 @@ void agft_step_kernel(StepArgs p) {
     // at D = 32 they would push the scalar registers into spills.
     __shared__ float s_x[D];
     if (wave == 0 && lane < D) s_x[lane] = decide ? p.ctx[(size_t)inst * D + lane] : 0.0f;
+    // the environment's state of this instance, fetched now for the epilogue
+    __shared__ uint32_t s_envw[ENV ? 32 : 1];
+    uint32_t env_pre = 0u;
+    if constexpr (ENV)
+        if (wave == 0) env_pre = agft_env_detail::env_prefetch(env, inst, lane);
     // This lane's selectors of x: xa_e = x_e for e <= j, xb_e = x_{D-e} for e > j.
     float xa[D + 1], xb[D + 1];
 #pragma unroll
@@ -1073,6 +1085,8 @@ void agft_step_kernel(StepArgs p) {
             }
         }
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
+        if constexpr (ENV)
+            if (wave == 0) agft_env_detail::env_epilogue(env, inst, -1, lane, env_pre, s_envw);
         write_back();
         return;
     }
@@ -1224,6 +1238,9 @@ void agft_step_kernel(StepArgs p) {
         if (ph_lane) blk[tid] = s_phw[tid - kInstMode];
         if (lane >= kInstX && lane < kInstX + D)
             reinterpret_cast<float *>(blk)[lane] = s_x[lane - kInstX];
+        // the context and reward read at the start are dead by now: the
+        // environment's response overwrites them in place
+        if constexpr (ENV) agft_env_detail::env_epilogue(env, inst, a, lane, env_pre, s_envw);
     }
     write_back();
 }
@@ -1401,12 +1418,100 @@ T *at(char *base, size_t off) {
 
 // The step kernel for one or four wavefronts per workgroup (the two widths
 // waves_for chooses), each compiled for its width.
-template <int D, int TF, int W>
-void launch_step(int waves, unsigned grid, size_t lds, hipStream_t stream, const StepArgs &p) {
+template <int D, int TF, int W, bool ENV>
+void launch_width(int waves, unsigned grid, size_t lds, hipStream_t stream, const StepArgs &p,
+                  const agft_env_detail::EnvArgs &e) {
     if (waves == 1)
-        hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 1>), dim3(grid), dim3(kWave), lds, stream, p);
+        hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 1, ENV>), dim3(grid), dim3(kWave), lds, stream, p, e);
     else
-        hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 4>), dim3(grid), dim3(4 * kWave), lds, stream, p);
+        hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 4, ENV>), dim3(grid), dim3(4 * kWave), lds, stream, p, e);
+}
+
+// One decision for every instance of handle h (and, with env, the
+// environment's response): arguments checked by the caller.
+int launch_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t *d_action, float *d_scores,
+                const agft_env_detail::EnvArgs *env) {
+    const agft_config &c = h->cfg;
+    StepArgs p;
+    p.arms = at<float4>(h->base, h->lay.arms);
+    p.mask = at<uint32_t>(h->base, h->lay.mask);
+    p.inst = at<int32_t>(h->base, h->lay.inst);
+    p.stats = at<int2>(h->base, h->lay.stats);
+    p.theta = c.exploit ? at<float>(h->base, h->lay.theta) : nullptr;
+    p.h.mask = c.prune_rule & 14;
+    p.h.ext_rounds = c.ext_rounds;
+    p.h.ext_min_n = c.ext_min_n;
+    p.h.ext_thr = c.ext_thr;
+    p.h.hist_after = c.hist_after;
+    p.h.hist_min_n = c.hist_min_n;
+    p.h.hist_kappa = c.hist_kappa;
+    p.h.hist_min_arms = c.hist_min_arms;
+    p.h.cascade_k = c.cascade_k;
+    p.t = h->t;
+    p.e.on = c.exploit;
+    p.e.delta = c.ph_delta;
+    p.e.lambda = c.ph_lambda;
+    p.e.window = c.ph_window;
+    p.e.min_rounds = c.ph_min_rounds;
+    p.rf.now = (c.refine && d_ctx != nullptr && h->t > 0 && h->t % c.refine_period == 0) ? 1 : 0;
+    p.rf.stat = h->t < c.refine_mature ? 1 : 0;
+    p.rf.half = c.refine_half;
+    p.rf.min_n = c.refine_min_n;
+    p.hdr = at<StateHeader>(h->base, 0);
+    p.ctx = d_ctx;
+    p.reward = d_reward;
+    p.action = d_ctx != nullptr ? d_action : nullptr;
+    p.scores = d_ctx != nullptr ? d_scores : nullptr;
+    p.B = c.B;
+    p.K = c.K;
+    p.KW = (c.K + 31) / 32;
+    p.IW = inst_words(c.d);
+    p.apply_update = h->pending;
+    const int64_t t = h->t;
+    p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
+    p.prune_reset = p.prune_now && !c.prune_sticky ? 1 : 0;
+    p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
+    p.t_next = d_ctx != nullptr ? t + 1 : t;
+    agft_launch_shape shape;
+    agft_launch_shape_for(&c, &shape);
+    const int waves = shape.waves;
+    p.early_update = shape.early_update;
+    p.keep_stats = stats_kept(c) ? 1 : 0;
+    if (waves != 1 && waves != 4) return AGFT_E_UNSUPPORTED;
+    const unsigned grid = (unsigned)c.B;
+    const size_t lds = step_lds_bytes(c.K);
+    const bool packed_tails = shape.tail_floats == 3;
+    hipStream_t s = h->stream;
+    agft_env_detail::EnvArgs e{};
+    if (env != nullptr) e = *env;
+#define AGFT_LAUNCH(D_, TF_, W_)                                                  \
+    (env != nullptr ? launch_width<D_, TF_, W_, true>(waves, grid, lds, s, p, e) \
+                    : launch_width<D_, TF_, W_, false>(waves, grid, lds, s, p, e))
+    switch (c.d) {
+        case 8:
+            if (packed_tails) AGFT_LAUNCH(8, 3, 7);
+            else AGFT_LAUNCH(8, 4, 7);
+            break;
+        case 16:
+            if (packed_tails && shape.simd_waves == 6) AGFT_LAUNCH(16, 3, 6);
+            else if (packed_tails) AGFT_LAUNCH(16, 3, 7);
+            else AGFT_LAUNCH(16, 4, 7);
+            break;
+        case 32:
+            if (packed_tails) AGFT_LAUNCH(32, 3, 4);
+            else AGFT_LAUNCH(32, 4, 4);
+            break;
+        default: return AGFT_E_UNSUPPORTED;
+    }
+#undef AGFT_LAUNCH
+    if (hipGetLastError() != hipSuccess) return AGFT_E_HIP;
+    if (d_ctx != nullptr) {
+        h->t = t + 1;
+        h->pending = 1;
+    } else {
+        h->pending = 0;
+    }
+    return AGFT_OK;
 }
 
 }  // namespace
@@ -1490,82 +1595,33 @@ int agft_create(const agft_config *cfg, void *d_state, size_t nbytes, void *stre
 int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t *d_action, float *d_scores) {
     if (h == nullptr) return AGFT_E_INVAL;
     if (h->pending && d_reward == nullptr) return AGFT_E_STATE;
-    const agft_config &c = h->cfg;
-    StepArgs p;
-    p.arms = at<float4>(h->base, h->lay.arms);
-    p.mask = at<uint32_t>(h->base, h->lay.mask);
-    p.inst = at<int32_t>(h->base, h->lay.inst);
-    p.stats = at<int2>(h->base, h->lay.stats);
-    p.theta = c.exploit ? at<float>(h->base, h->lay.theta) : nullptr;
-    p.h.mask = c.prune_rule & 14;
-    p.h.ext_rounds = c.ext_rounds;
-    p.h.ext_min_n = c.ext_min_n;
-    p.h.ext_thr = c.ext_thr;
-    p.h.hist_after = c.hist_after;
-    p.h.hist_min_n = c.hist_min_n;
-    p.h.hist_kappa = c.hist_kappa;
-    p.h.hist_min_arms = c.hist_min_arms;
-    p.h.cascade_k = c.cascade_k;
-    p.t = h->t;
-    p.e.on = c.exploit;
-    p.e.delta = c.ph_delta;
-    p.e.lambda = c.ph_lambda;
-    p.e.window = c.ph_window;
-    p.e.min_rounds = c.ph_min_rounds;
-    p.rf.now = (c.refine && d_ctx != nullptr && h->t > 0 && h->t % c.refine_period == 0) ? 1 : 0;
-    p.rf.stat = h->t < c.refine_mature ? 1 : 0;
-    p.rf.half = c.refine_half;
-    p.rf.min_n = c.refine_min_n;
-    p.hdr = at<StateHeader>(h->base, 0);
-    p.ctx = d_ctx;
-    p.reward = d_reward;
-    p.action = d_ctx != nullptr ? d_action : nullptr;
-    p.scores = d_ctx != nullptr ? d_scores : nullptr;
-    p.B = c.B;
-    p.K = c.K;
-    p.KW = (c.K + 31) / 32;
-    p.IW = inst_words(c.d);
-    p.apply_update = h->pending;
-    const int64_t t = h->t;
-    p.prune_now = (d_ctx != nullptr && (c.prune_rule & 1) && t > 0 && t % c.prune_period == 0) ? 1 : 0;
-    p.prune_reset = p.prune_now && !c.prune_sticky ? 1 : 0;
-    p.alpha = c.alpha_sched == 0 ? c.alpha0 : (float)((double)c.alpha0 / std::sqrt((double)t + 1.0));
-    p.t_next = d_ctx != nullptr ? t + 1 : t;
-    agft_launch_shape shape;
-    agft_launch_shape_for(&c, &shape);
-    const int waves = shape.waves;
-    p.early_update = shape.early_update;
-    p.keep_stats = stats_kept(c) ? 1 : 0;
-    if (waves != 1 && waves != 4) return AGFT_E_UNSUPPORTED;
-    const unsigned grid = (unsigned)c.B;
-    const size_t lds = step_lds_bytes(c.K);
-    const bool packed_tails = shape.tail_floats == 3;
-    hipStream_t s = h->stream;
-    switch (c.d) {
-        case 8:
-            if (packed_tails) launch_step<8, 3, 7>(waves, grid, lds, s, p);
-            else launch_step<8, 4, 7>(waves, grid, lds, s, p);
-            break;
-        case 16:
-            if (packed_tails && shape.simd_waves == 6) launch_step<16, 3, 6>(waves, grid, lds, s, p);
-            else if (packed_tails) launch_step<16, 3, 7>(waves, grid, lds, s, p);
-            else launch_step<16, 4, 7>(waves, grid, lds, s, p);
-            break;
-        case 32:
-            if (packed_tails) launch_step<32, 3, 4>(waves, grid, lds, s, p);
-            else launch_step<32, 4, 4>(waves, grid, lds, s, p);
-            break;
-        default: return AGFT_E_UNSUPPORTED;
-    }
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return AGFT_E_HIP;
-    if (d_ctx != nullptr) {
-        h->t = t + 1;
-        h->pending = 1;
-    } else {
-        h->pending = 0;
-    }
-    return AGFT_OK;
+    return launch_step(h, d_ctx, d_reward, d_action, d_scores, nullptr);
+}
+
+int agft_sim_step(agft_handle *h, const agft_env_config *env_cfg, void *d_env, size_t env_nbytes,
+                  const int32_t *d_arrivals, const float *d_noise, float *d_ctx, float *d_reward,
+                  int32_t *d_action, float *d_scores) {
+    using namespace agft_env_detail;
+    if (h == nullptr || !env_config_ok(env_cfg)) return AGFT_E_INVAL;
+    if (env_cfg->B != h->cfg.B || env_cfg->K != h->cfg.K || env_cfg->d != h->cfg.d) return AGFT_E_INVAL;
+    if (d_env == nullptr || d_arrivals == nullptr || d_noise == nullptr || d_ctx == nullptr ||
+        d_reward == nullptr || d_action == nullptr)
+        return AGFT_E_INVAL;
+    if (reinterpret_cast<uintptr_t>(d_ctx) % 16 != 0) return AGFT_E_INVAL;
+    if (reinterpret_cast<uintptr_t>(d_env) % agft_env_detail::kAlign != 0 || env_nbytes < env_layout(env_cfg->B).total)
+        return AGFT_E_INVAL;
+    if (h->t >= env_cfg->T) return AGFT_E_STATE;   // the draws end at window T
+    EnvArgs e = make_args(env_cfg, d_env);
+    e.arrivals = d_arrivals;
+    e.noise = d_noise;
+    e.action = d_action;
+    e.reward = d_reward;
+    e.ctx = d_ctx;
+    e.w = (int32_t)h->t + 1;
+    const double tau = env_cfg->T > 1 ? (double)h->t / (double)(env_cfg->T - 1) : 0.0;
+    e.scale = (float)(1.0 + (double)env_cfg->drift * tau);
+    e.reset = 0;
+    return launch_step(h, d_ctx, d_reward, d_action, d_scores, &e);
 }
 
 int agft_launch_shape_for(const agft_config *cfg, agft_launch_shape *out) {

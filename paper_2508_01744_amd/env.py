@@ -44,7 +44,8 @@ class GpuEnv:
         self.nbytes = L.agft_env_state_bytes(cfg)
         if self.nbytes == 0:
             raise ValueError("invalid environment configuration")
-        self.state = torch.empty(self.nbytes, dtype=torch.uint8, device=dev)
+        # zeroed so that the alignment gaps between regions are deterministic
+        self.state = torch.zeros(self.nbytes, dtype=torch.uint8, device=dev)
         self.ctx = torch.empty(self.B, self.d, dtype=torch.float32, device=dev)
         self.reward = torch.empty(self.B, dtype=torch.float32, device=dev)
         self.stream = stream if stream is not None else torch.cuda.current_stream(dev)
@@ -63,4 +64,15 @@ class GpuEnv:
                                                  _ptr(action), _ptr(self.arrivals),
                                                  _ptr(self.noise), _ptr(self.reward),
                                                  _ptr(self.ctx), self._s()))
+        return self.reward, self.ctx
+
+    def fused_step(self, tuner, action, scores=None):
+        """One decision of tuner (agft_step) and this environment's response
+        to it, in one launch (agft_sim_step): self.ctx and self.reward hold
+        x_t and r_{t-1} on entry and x_{t+1} and r_t on return."""
+        tuner._check(action, (self.B,), torch.int32)
+        tuner._check(scores, (self.B, 2, tuner.K), torch.float32)
+        L.check("agft_sim_step", L.agft_sim_step(tuner.h, self.cfg, _ptr(self.state), self.nbytes,
+                                                 _ptr(self.arrivals), _ptr(self.noise), _ptr(self.ctx),
+                                                 _ptr(self.reward), _ptr(action), _ptr(scores)))
         return self.reward, self.ctx

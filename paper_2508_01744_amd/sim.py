@@ -7,10 +7,12 @@ from .tuner import Tuner
 
 
 def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, scores=False,
-                    device="cuda"):
+                    device="cuda", fused=False):
     """Run T decisions of wl.B instances.
 
     arrivals, noise: [T+1][B] (numpy or torch) exogenous draws.
+    fused: each decision and the environment's response in one launch
+    (agft_sim_step) instead of two (agft_step, agft_env_step).
     probes: instance indices to record at every step (contexts, rewards,
     actions, masks, test words, action spaces; with scores, the scores and
     the top-two gap of each decision); the records are returned as host
@@ -42,9 +44,13 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
     x = env.reset()
     r = None
     for t in range(T):
-        tuner.step(x, r, action, sc)
         if rec is not None:
             rec["x"][t] = x.index_select(0, pidx)
+        if fused:
+            r, x = env.fused_step(tuner, action, sc)
+        else:
+            tuner.step(x, r, action, sc)
+        if rec is not None:
             rec["a"][t] = action.index_select(0, pidx)
             rec["mask"][t] = view["mask"].index_select(0, pidx)
             rec["kact"][t] = view["kact"].index_select(0, pidx)
@@ -53,7 +59,8 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
             if scores:
                 rec["scores"][t] = sc.index_select(0, pidx)
                 rec["gap"][t] = view["gap"].index_select(0, pidx)
-        r, x = env.step(t, action)
+        if not fused:
+            r, x = env.step(t, action)
         if rec is not None:
             rec["r"][t] = r.index_select(0, pidx)
     tuner.flush(r)

@@ -164,6 +164,17 @@ def test_env_validation(lib):
     assert L.agft_env_step(cfg, p, n, 0, p, p, p, p, q, None) == L.AGFT_E_INVAL
 
 
+def test_sim_step_rejects_before_launch(lib):
+    """agft_sim_step checks its arguments before anything is enqueued: no
+    handle, a missing buffer, an environment of another shape."""
+    cfg = _env_cfg()
+    n = L.agft_env_state_bytes(cfg)
+    p = ctypes.c_void_p(0x100000)
+    assert L.agft_sim_step(None, cfg, p, n, p, p, p, p, p, None) == L.AGFT_E_INVAL
+    bad = _env_cfg(d=7)
+    assert L.agft_sim_step(None, bad, p, n, p, p, p, p, p, None) == L.AGFT_E_INVAL
+
+
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     """No silent fallback: without the built library every entry point raises."""
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "libagft.so"))

@@ -22,8 +22,9 @@ def test_step_kernels_do_not_spill(tmp_path):
     out = subprocess.run(cmd, capture_output=True, text=True, check=True).stderr
     kernels = re.findall(r"Function Name: (\S*agft_step_kernel\S*)(.*?)(?=Function Name:|\Z)", out, re.S)
     # d = 8, 16, 32, each with packed and padded tails; d = 16 packed also at
-    # six wavefronts per SIMD; each for one- and four-wavefront workgroups
-    assert len(kernels) == 14, out[-2000:]
+    # six wavefronts per SIMD; each for one- and four-wavefront workgroups,
+    # with and without the simulator's environment in the epilogue
+    assert len(kernels) == 28, out[-2000:]
     for name, body in kernels:
         scratch = int(re.search(r"ScratchSize \[bytes/lane\]: (\d+)", body).group(1))
         assert scratch == 0, f"{name} spills {scratch} bytes per lane"
