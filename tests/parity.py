@@ -32,7 +32,8 @@ import numpy as np
 from agft_workloads import exogenous
 from oracle import Oracle, run_closed_loop
 
-SCORE_TOL = 1e-4   # |s_gpu - s_oracle| <= SCORE_TOL * max(1, |s_oracle|)
+SCORE_TOL = 1e-4   # |s_gpu - s_oracle| <= SCORE_TOL * max(1, |s_oracle|): relative for |s| >= 1,
+                   # absolute below (rewards and scores are O(1), many below 1 in magnitude)
 TIE = 1e-5         # score gaps at or below this (times max(1, |score|)) are near-ties
 ENV_TOL = 1e-5     # contexts and rewards: fp32 environment vs fp64 environment
 PH_TOL = 1e-4      # Page-Hinkley running sums: |s_gpu - s_oracle| <= PH_TOL * max(1, |s_oracle|)
@@ -76,7 +77,8 @@ class Checker:
         self.st = dict(max_score_err=0.0, max_ctx_err=0.0, max_reward_err=0.0, forced=0,
                        forced_prune=0, forced_rules=0, exact_tie_steps=0, decisions=0,
                        no_decision=0, max_ph_err=0.0, forced_ph=0, forced_mode=0,
-                       greedy_decisions=0, refinements=0, forced_window=0, max_gap_err=0.0)
+                       greedy_decisions=0, refinements=0, forced_window=0, max_gap_err=0.0,
+                       max_rel_err_abs_ge_1=0.0, max_abs_err_abs_lt_1=0.0)
 
     def _anchor(self, lo, hi):
         h = self.refine["refine_half"]
@@ -203,6 +205,14 @@ class Checker:
                         err = np.where(act[i], np.abs(self.g_s[t, i, row] - ref) / np.maximum(1.0, np.abs(ref)),
                                        0.0)
                     st["max_score_err"] = max(st["max_score_err"], float(err.max()))
+                    # the same errors split by magnitude: relative where |s| >= 1,
+                    # absolute below (where the bar's floor of 1 makes it absolute)
+                    big = act[i] & (np.abs(ref) >= 1.0)
+                    if big.any():
+                        st["max_rel_err_abs_ge_1"] = max(st["max_rel_err_abs_ge_1"], float(err[big].max()))
+                    small = act[i] & ~big
+                    if small.any():
+                        st["max_abs_err_abs_lt_1"] = max(st["max_abs_err_abs_lt_1"], float(err[small].max()))
                     if err.max() > SCORE_TOL:
                         k = int(np.argmax(err))
                         self.fail(f"score mismatch at t={t}, instance {ids[i]}, arm {k}: "

@@ -5,15 +5,15 @@ and cfg5 (1,024), every fourth of cfg3 and every sixteenth of cfg4 (4,096
 each, the last instance included), closed loop, at every step: contexts,
 rewards, prune decisions and actions (identical except at near-ties), then
 the final models.  The same for their variants with the paper's pruning
-rules (cfg2p ... cfg5p).  (cfg1 is a single instance, compared in full by
-the parity tests.)
+rules (cfg2p ... cfg5p), with the switch to exploitation (cfg2e ... cfg5e,
+with the test state after every step), with the refinement (cfg2r ...
+cfg5r, with the action space after every step), cfg4pe, cfg4per, and with
+rule 1 re-evaluated (cfg3n ... cfg5n).  (cfg1 is a single instance, compared
+in full by the parity tests.)
 
 With AGFT_EVERY_INSTANCE=1 (minutes of oracle time on the host, so not part
-of the default run), the same for the variants with the switch to
-exploitation (cfg2e ... cfg5e, with the test state after every step), the
-refinement (cfg2r ... cfg5r, with the action space after every step),
-cfg4pe and cfg4per; and every instance of cfg3 (16,384) and cfg4 (65,536),
-in parts that share one GPU run per workload."""
+of the default run): every instance of cfg3 (16,384) and cfg4 (65,536), in
+parts that share one GPU run per workload."""
 import os
 
 import numpy as np
@@ -28,7 +28,7 @@ from paper_2508_01744_amd import run_closed_loop
 pytestmark = pytest.mark.gpu
 
 STRIDE = {f"cfg{n}{v}": {2: 1, 3: 4, 4: 16, 5: 1}[n] for n in (2, 3, 4, 5) for v in ("", "p", "e", "r")}
-STRIDE.update(cfg4pe=16, cfg4per=16)
+STRIDE.update(cfg4pe=16, cfg4per=16, cfg3n=4, cfg4n=16, cfg5n=1)
 EVERY = os.environ.get("AGFT_EVERY_INSTANCE") == "1"
 OPT_IN = "set AGFT_EVERY_INSTANCE=1 (minutes of oracle time)"
 FIELDS = ("a", "mask", "x", "r", "ph", "win")
@@ -36,8 +36,6 @@ FIELDS = ("a", "mask", "x", "r", "ph", "win")
 
 @pytest.mark.parametrize("name", sorted(STRIDE))
 def test_many_instances_full_size(name):
-    if name[4:] not in ("", "p") and not EVERY:
-        pytest.skip(OPT_IN)
     wl = get_workload(name)
     ids = list(range(0, wl.B, STRIDE[name]))
     if ids[-1] != wl.B - 1:

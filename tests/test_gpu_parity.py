@@ -26,7 +26,8 @@ def _run_and_compare(wl, probes):
     out = run_closed_loop(wl, ENV, arr, noi, probes=probes, scores=True)
     st = parity.compare(wl, wl.T, probes, out["probes"])
     wth, wai = compare_model(out["tuner"], st["oracle"], probes, THETA_TOL, AINV_TOL)
-    say(f"[parity] {wl.name}: max score err {st['max_score_err']:.2e}, ctx err "
+    say(f"[parity] {wl.name}: max score err {st['max_score_err']:.2e} (relative, |s| >= 1: "
+        f"{st['max_rel_err_abs_ge_1']:.2e}; absolute, |s| < 1: {st['max_abs_err_abs_lt_1']:.2e}), ctx err "
         f"{st['max_ctx_err']:.2e}, reward err {st['max_reward_err']:.2e}, forced "
         f"{st['forced']}/{st['decisions']}, prune forced {st['forced_prune']}, rules forced "
         f"{st['forced_rules']}, exact-tie steps "
