@@ -316,6 +316,39 @@ def copy_rate(dev, reps):
     return gbs
 
 
+CEILING_LIB = os.path.join(ROOT, "paper_2508_01744_amd", "libagft_ceiling.so")
+
+
+def stream_ceiling(wl, launches=20):
+    """The attainable rate of this workload's step traffic without its
+    arithmetic (libagft_ceiling.so): one workgroup per instance reads every
+    chunk of an instance-sized region of the step kernel's record layout,
+    then, in the second form, writes one record back, as the step's update
+    does.  Returns both rates in GB/s (bytes moved over the average launch
+    duration) and the durations."""
+    import ctypes
+    from paper_2508_01744_amd import launch_shape, workload_config
+    if not os.path.exists(CEILING_LIB):
+        raise RuntimeError(f"{CEILING_LIB} is not built: run __graft_entry__.build()")
+    lib = ctypes.CDLL(CEILING_LIB)
+    lib.agft_stream_ceiling.restype = ctypes.c_int
+    lib.agft_stream_ceiling.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    tf = launch_shape(workload_config(wl))["tail_floats"]
+    nb = 64 // wl.d
+    rec = (wl.d // 2) * (wl.d // 4) + (wl.d // 2) * tf // 4      # 16-byte chunks per arm record
+    chunks = -(-wl.K // nb) * nb * rec                           # per instance, blocks of nb arms
+    r_us, rw_us = ctypes.c_double(), ctypes.c_double()
+    code = lib.agft_stream_ceiling(wl.B, chunks, rec, launches, ctypes.byref(r_us), ctypes.byref(rw_us))
+    if code != 0:
+        raise RuntimeError(f"agft_stream_ceiling failed ({code})")
+    read_b, write_b = wl.B * chunks * 16, wl.B * rec * 16
+    return {"read_gbs": read_b / (r_us.value * 1e-6) / 1e9,
+            "read_writeback_gbs": (read_b + write_b) / (rw_us.value * 1e-6) / 1e9,
+            "read_us": r_us.value, "read_writeback_us": rw_us.value,
+            "bytes_per_launch": read_b, "writeback_bytes_per_launch": write_b, "launches": launches}
+
+
 # the other workloads, timed over their whole horizon beside the headline
 DETAIL_WORKLOADS = ("cfg1", "cfg2", "cfg3", "cfg4", "cfg5")
 
@@ -330,6 +363,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-workloads", action="store_true",
                     help="skip the runs of the other workloads reported under detail.workloads")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the stream-ceiling measurement reported under roofline.ceiling")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="time the plain 1 GiB copy 3 times instead of 5 (for counter calibration runs)")
     args = ap.parse_args()
@@ -352,6 +387,8 @@ def main():
     draws = exogenous(wl, T=max(K, W, wl.T if wl.name in DETAIL_WORKLOADS else 1, 1))
     head = measure(wl, K, W, dev, draws=draws)
     copy_gbs = copy_rate(dev, 3 if args.calibrate_copy else 5)
+    torch.cuda.synchronize()
+    ceiling = None if args.no_ceiling else stream_ceiling(wl)
     traffic = counter_traffic(wl.name, steps=K, warmup=W)
 
     res = {
@@ -381,6 +418,14 @@ def main():
                                         "mean_active_arms_after_step", "exploiting_fraction", "wall_s")},
     }
     res["detail"]["device_copy_gbs"] = copy_gbs
+    if ceiling is not None:
+        res["roofline"]["ceiling"] = {
+            "read_gbs": ceiling["read_gbs"], "read_writeback_gbs": ceiling["read_writeback_gbs"],
+            "achieved_over_read_writeback": head["achieved_gbs"] / ceiling["read_writeback_gbs"],
+            "what": (f"the step's traffic without its arithmetic on {wl.name}'s record layout "
+                     f"({ceiling['bytes_per_launch'] / wl.B:.0f} B read per instance, one "
+                     f"{ceiling['writeback_bytes_per_launch'] / wl.B:.0f} B record written back), one workgroup "
+                     f"per instance, non-temporal loads and stores; average of {ceiling['launches']} launches")}
     if not args.no_workloads:
         runs = {}
         for name in DETAIL_WORKLOADS:

@@ -29,6 +29,23 @@ def build(verbose=False, extra_flags=()):
     return LIB
 
 
+# the stream-ceiling measurement (bench.py), a library of its own
+CEILING_SRC = os.path.join(CSRC, "stream_ceiling.hip")
+CEILING_LIB = os.path.join(PKG, "libagft_ceiling.so")
+
+
+def build_ceiling(verbose=False):
+    """Compile the stream-ceiling kernels into paper_2508_01744_amd/libagft_ceiling.so."""
+    hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    tmp = CEILING_LIB + ".tmp"
+    cmd = [hipcc, *HIPCC_FLAGS, CEILING_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, CEILING_LIB)
+    return CEILING_LIB
+
+
 C_EXAMPLE_SRC = os.path.join(ROOT, "tests", "c_abi", "agft_c_example.c")
 C_EXAMPLE = os.path.join(ROOT, "tests", "c_abi", "agft_c_example")
 
@@ -49,3 +66,4 @@ def build_c_example(verbose=False):
 
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_ceiling(verbose=True))

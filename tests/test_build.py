@@ -1,6 +1,7 @@
-"""Build-level guard (CPU): the step kernels compile for gfx950 without
-register spills.  A spill puts per-lane scratch traffic into the streaming
-loop, which costs bandwidth the step cannot spare."""
+"""Build-level guards (CPU): the step kernels compile for gfx950 without
+register spills (a spill puts per-lane scratch traffic into the streaming
+loop, which costs bandwidth the step cannot spare), and the bench's
+stream-ceiling library is built and checks its arguments."""
 import os
 import re
 import shutil
@@ -28,3 +29,20 @@ def test_step_kernels_do_not_spill(tmp_path):
     for name, body in kernels:
         scratch = int(re.search(r"ScratchSize \[bytes/lane\]: (\d+)", body).group(1))
         assert scratch == 0, f"{name} spills {scratch} bytes per lane"
+
+
+def test_stream_ceiling_library_checks_its_arguments():
+    """The bench's ceiling library is built beside the tuner's, exports its
+    one entry point and rejects out-of-range arguments before any HIP call."""
+    import ctypes
+    assert os.path.exists(_build.CEILING_LIB), "run __graft_entry__.build()"
+    lib = ctypes.CDLL(_build.CEILING_LIB)
+    f = lib.agft_stream_ceiling
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    a, b = ctypes.c_double(), ctypes.c_double()
+    for args in ((0, 4864, 38, 1), (1 << 31, 4864, 38, 1), (1, 0, 1, 1), (1, 4864, 0, 1), (1, 4864, 257, 1),
+                 (1, 10, 38, 1), (1, 4864, 38, 0)):
+        assert f(*args, ctypes.byref(a), ctypes.byref(b)) == 1, args
+    assert f(1, 4864, 38, 1, None, ctypes.byref(b)) == 1

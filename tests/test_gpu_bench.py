@@ -43,6 +43,12 @@ def test_bench_json_line():
     assert cb["cores"] >= 1 and "cfg2" in cb["sample"]
     assert det["cpu_oracle_1thread"]["cores"] == 1
     assert rf["byte_model"]["model_bytes_per_arm"] == 176 and rf["byte_model"]["dense_bytes_per_arm"] == 288
+    # the stream ceiling on cfg2's layout: reading alone is faster than
+    # reading plus the write-back, and the step kernel reaches neither
+    ce = rf["ceiling"]
+    assert ce["read_gbs"] > 0 and ce["read_writeback_gbs"] > 0
+    assert abs(ce["achieved_over_read_writeback"] - rf["achieved"] / ce["read_writeback_gbs"]) < 1e-9
+    assert 0 < ce["achieved_over_read_writeback"] < 1.2 and "cfg2" in ce["what"]
     # every workload over its whole horizon beside the headline
     wls = det["workloads"]
     assert set(wls) == {"cfg1", "cfg2", "cfg3", "cfg4", "cfg5"}
