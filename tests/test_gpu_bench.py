@@ -49,6 +49,9 @@ def test_bench_json_line():
     assert ce["read_gbs"] > 0 and ce["read_writeback_gbs"] > 0
     assert abs(ce["achieved_over_read_writeback"] - rf["achieved"] / ce["read_writeback_gbs"]) < 1e-9
     assert 0 < ce["achieved_over_read_writeback"] < 1.2 and "cfg2" in ce["what"]
+    for when in ("after_headline", "after_idle"):
+        assert 0 < ce[when]["read_writeback_gbs"] <= ce["read_writeback_gbs"]
+        assert 0 < ce[when]["read_gbs"] <= ce["read_gbs"]
     # every workload over its whole horizon beside the headline
     wls = det["workloads"]
     assert set(wls) == {"cfg1", "cfg2", "cfg3", "cfg4", "cfg5"}
