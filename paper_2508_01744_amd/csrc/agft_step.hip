@@ -949,10 +949,44 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
                     make_int2(s_stu.x + 1, __float_as_int(__int_as_float(s_stu.y) + r));
         }
     };
+    // The updated arm, scored on x_t from LDS exactly as the stream scores a
+    // record from HBM (same slices, same operation order).  With the early
+    // update it runs right after it, while the stream's first pass is in
+    // flight, instead of after the stream on the step's critical path.
+    auto score_updated = [&]() {
+        if (upd && x_ok && wave == 0) {
+            float f[4 * S];
+#pragma unroll
+            for (int sidx = 0; sidx < R::MQ; ++sidx) {
+                const float4 c4 = s_new4[sidx * G + j];
+                f[4 * sidx] = c4.x;
+                f[4 * sidx + 1] = c4.y;
+                f[4 * sidx + 2] = c4.z;
+                f[4 * sidx + 3] = c4.w;
+            }
+            const float *tl = s_new + 4 * R::MAIN + TF * j;
+            f[4 * R::MQ] = tl[0];
+            f[4 * R::MQ + 1] = tl[1];
+            f[4 * R::MQ + 2] = tl[2];
+            f[4 * R::MQ + 3] = 0.0f;
+            float m, w2;
+            slice_terms<D>(f, xa, xb, xt0, xt1, m, w2);
+            m = group_sum<G>(m);
+            w2 = group_sum<G>(w2);
+            if (lane == 0) {
+                const float w = sqrtf(w2);
+                s_ucb[a_upd] = greedy ? m : fmaf(p.alpha, w, m);
+                s_lcb[a_upd] = greedy ? m : fmaf(-p.alpha, w, m);
+            }
+        }
+    };
     // An exploiting instance has no pass in flight.  Where the whole list fits
     // in the first pass, no later pass can wait behind the update.
     const bool early = (p.early_update || nlist <= apw) && !greedy;
-    if (early) update();
+    if (early) {
+        update();
+        score_updated();
+    }
 
     // ---- scoring of every listed arm (Eq. 1), two passes in flight ----
     if (greedy) {
@@ -1026,36 +1060,10 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
         }
     }
 
-    if (!early) update();
-
-    // the updated arm, scored on x_t from LDS exactly as the stream scores a
-    // record from HBM (same slices, same operation order)
-    if (upd && x_ok && wave == 0) {
-        float f[4 * S];
-#pragma unroll
-        for (int sidx = 0; sidx < R::MQ; ++sidx) {
-            const float4 c4 = s_new4[sidx * G + j];
-            f[4 * sidx] = c4.x;
-            f[4 * sidx + 1] = c4.y;
-            f[4 * sidx + 2] = c4.z;
-            f[4 * sidx + 3] = c4.w;
-        }
-        const float *tl = s_new + 4 * R::MAIN + TF * j;
-        f[4 * R::MQ] = tl[0];
-        f[4 * R::MQ + 1] = tl[1];
-        f[4 * R::MQ + 2] = tl[2];
-        f[4 * R::MQ + 3] = 0.0f;
-        float m, w2;
-        slice_terms<D>(f, xa, xb, xt0, xt1, m, w2);
-        m = group_sum<G>(m);
-        w2 = group_sum<G>(w2);
-        if (lane == 0) {
-            const float w = sqrtf(w2);
-            s_ucb[a_upd] = greedy ? m : fmaf(p.alpha, w, m);
-            s_lcb[a_upd] = greedy ? m : fmaf(-p.alpha, w, m);
-        }
+    if (!early) {
+        update();
+        score_updated();
     }
-
 
     if (!decide) {
         if (tid == 0) {
