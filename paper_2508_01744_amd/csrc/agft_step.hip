@@ -23,8 +23,9 @@
 //      instance reads only a contiguous copy of theta and scores m (Eq. 2);
 //   3. fold the previous decision's reward into its arm: Eq. 3-5 as a
 //      square-root rank-1 update of S (below) plus the matching theta
-//      update, staged in LDS and written back; the updated arm is scored on
-//      x_t from LDS in the same operation order as the stream;
+//      update, in LDS while the stream's first pass is in flight; the
+//      updated arm is scored on x_t from LDS in the same operation order as
+//      the stream, and its record is written back at the end of the step;
 //   4. pruning when due (drop UCB_k < max_j LCB_j), argmax with ties to the
 //      lowest arm index; refinement of the action space when due; epilogue.
 //
@@ -673,9 +674,8 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
                                : __float_as_int(pick<6>(ph, tid - kInstPh));
 
     // Record of the previous decision's arm: fetched now, staged in LDS before the stream.
-    // Its reward count and sum are fetched now as well: read at update time
-    // they would wait behind the record's write-back (stores and loads share
-    // one completion counter), about 6 us per workgroup.
+    // Its reward count and sum are fetched with it, so that the end of the
+    // step only stores them.
     float4 old_chunk[NQ];
     int2 st_upd = make_int2(0, 0);
     if (upd) {
