@@ -394,10 +394,17 @@ def main():
     # compared with the faster of the two (run before the headline, the
     # ceiling's own load would slow the headline down)
     ceil_busy = ceil_idle = None
+    ceil_error = None
     if not args.no_ceiling:
-        ceil_busy = stream_ceiling(wl)
-        time.sleep(1.0)
-        ceil_idle = stream_ceiling(wl)
+        # a side measurement: if it cannot run, the line says why and stands
+        try:
+            ceil_busy = stream_ceiling(wl)
+            time.sleep(1.0)
+            ceil_idle = stream_ceiling(wl)
+        except (OSError, RuntimeError) as exc:
+            ceil_busy = ceil_idle = None
+            ceil_error = str(exc)
+            log(f"[bench] stream ceiling not measured: {exc}")
     traffic = counter_traffic(wl.name, steps=K, warmup=W)
 
     res = {
@@ -427,6 +434,8 @@ def main():
                                         "mean_active_arms_after_step", "exploiting_fraction", "wall_s")},
     }
     res["detail"]["device_copy_gbs"] = copy_gbs
+    if ceil_error is not None:
+        res["roofline"]["ceiling"] = {"error": ceil_error}
     if ceil_busy is not None:
         c0, c1 = ceil_busy, ceil_idle
         rw = max(c0["read_writeback_gbs"], c1["read_writeback_gbs"])

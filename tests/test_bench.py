@@ -1,11 +1,14 @@
 """bench.py's contract on the CPU: the one-GPU guard, the algorithmic byte
 count the roofline divides by, the rule that measured traffic is reported
 only for the kernel source and workload it was taken on, and the fields of
-the oracle baselines."""
+the oracle baselines, and that the stream ceiling's failure is reported, not
+fatal."""
 import json
 import os
 import subprocess
 import sys
+
+import pytest
 
 import bench
 from agft_workloads import get_workload
@@ -81,3 +84,12 @@ def test_byte_model_states_both_layouts():
     assert bm["model_bytes_per_arm"] == 608 and bm["dense_bytes_per_arm"] == 1088
     bm = bench.byte_model(get_workload("cfg5"))
     assert bm["model_bytes_per_arm"] == 4 * (32 + 528) and bm["dense_bytes_per_arm"] == 4 * (1024 + 32)
+
+
+def test_ceiling_failure_does_not_sink_the_line(monkeypatch):
+    """The stream ceiling is a side measurement: if its library cannot run,
+    stream_ceiling raises a RuntimeError that main() records in the line."""
+    monkeypatch.setattr(bench, "CEILING_LIB", "/nonexistent/libagft_ceiling.so")
+    wl = get_workload("cfg2")
+    with pytest.raises(RuntimeError, match="not built"):
+        bench.stream_ceiling(wl)
