@@ -166,6 +166,22 @@ def cpu_baseline(wl, budget_s, threads=None, n_max=16384, max_steps=None):
                        f"environment, {el:.1f} s)", n=n, steps=steps)
 
 
+def host_cpu():
+    """The host processor the oracle baseline ran on: model name, logical
+    CPUs visible to this process and in the machine."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    visible = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"model": model, "cpus_visible": visible, "cpus_machine": os.cpu_count()}
+
+
 def measure(wl, K, W, dev, log_prefix="[bench]", draws=None):
     """Run W untimed warm-up steps of workload wl, re-initialise, time K steps
     from the fresh state (the step and environment kernels of each step),
@@ -479,6 +495,7 @@ def main():
                            n_max=max(1, base["n"] // (3 * base["cores"])))
         res["cpu_baseline"] = {k: base[k] for k in ("value", "unit", "cores", "kind", "sample")}
         res["detail"]["cpu_oracle_1thread"] = {k: one[k] for k in ("value", "unit", "cores", "sample")}
+        res["detail"]["host_cpu"] = host_cpu()
     print(json.dumps(res), flush=True)
 
 

@@ -93,3 +93,9 @@ def test_ceiling_failure_does_not_sink_the_line(monkeypatch):
     wl = get_workload("cfg2")
     with pytest.raises(RuntimeError, match="not built"):
         bench.stream_ceiling(wl)
+
+
+def test_host_cpu_is_described():
+    h = bench.host_cpu()
+    assert h["cpus_visible"] >= 1 and h["cpus_machine"] >= h["cpus_visible"]
+    assert h["model"] is None or isinstance(h["model"], str)
