@@ -181,6 +181,48 @@ static_assert(rec_pos_consistent<8, 3>() && rec_pos_consistent<8, 4>() && rec_po
                   rec_pos_consistent<16, 4>() && rec_pos_consistent<32, 3>() && rec_pos_consistent<32, 4>(),
               "record offsets of the update disagree with the record layout");
 
+// The update walks the factor RP rows apart from one pass to the next.  For
+// RP a multiple of 4, row r0 + ps*RP of column jc sits at a fixed per-lane
+// base plus ps steps of +G*RP floats (top-down slices, columns < G) or
+// -G*RP (bottom-up slices), except row 0 of a bottom-up column, which is its
+// slice's tail float; theta_i, RP/2 slices further per pass, moves by TF*RP/2.
+// So each pass costs one add of address arithmetic.  Checked at compile time
+// against rec_pos_S for every lane and pass of the kernels' shapes.
+template <int D, int TF, int RP>
+struct RowWalk {
+    static constexpr int G = D / 2, MAIN = G * (D / 4);
+    static constexpr bool kLinear = RP % 4 == 0;
+    __host__ __device__ static constexpr int step(int jc) { return jc < G ? G * RP : -G * RP; }
+    __host__ __device__ static constexpr int base(int r0, int jc) {
+        const int sl = jc < G ? jc : D - 1 - jc;
+        const int e = jc < G ? r0 : D - r0;
+        return 4 * ((e >> 2) * G + sl) + (e & 3);
+    }
+    __host__ __device__ static constexpr int tail(int jc) { return 4 * MAIN + TF * (D - 1 - jc); }
+    __host__ __device__ static constexpr int pos(int r0, int jc, int ps) {
+        return ps == 0 && r0 == 0 && jc >= G ? tail(jc) : base(r0, jc) + ps * step(jc);
+    }
+};
+
+template <int D, int TF, int RP>
+constexpr bool row_walk_consistent() {
+    if constexpr (!RowWalk<D, TF, RP>::kLinear) return true;
+    for (int jc = 0; jc < D; ++jc)
+        for (int r0 = 0; r0 < RP && r0 < D; ++r0)
+            for (int ps = 0; r0 + ps * RP < D; ++ps) {
+                const int i = r0 + ps * RP;
+                if (i <= jc && RowWalk<D, TF, RP>::pos(r0, jc, ps) != rec_pos_S<D, TF>(i, jc)) return false;
+                if (rec_pos_theta<D, TF>(r0) + ps * TF * (RP / 2) != rec_pos_theta<D, TF>(i)) return false;
+            }
+    return true;
+}
+// rows per pass: (64 / D) segments per wavefront times 1 or 4 wavefronts
+static_assert(row_walk_consistent<8, 3, 8>() && row_walk_consistent<8, 4, 8>() && row_walk_consistent<8, 3, 32>() &&
+                  row_walk_consistent<8, 4, 32>() && row_walk_consistent<16, 3, 4>() && row_walk_consistent<16, 4, 4>() &&
+                  row_walk_consistent<16, 3, 16>() && row_walk_consistent<16, 4, 16>() &&
+                  row_walk_consistent<32, 3, 8>() && row_walk_consistent<32, 4, 8>(),
+              "the update's row walk matches the record layout");
+
 // Column j and row i of packed element e.
 __device__ inline void unpack(int e, int &i, int &j) {
     int c = 0;
@@ -870,13 +912,21 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
             // segment-wide DPP reductions instead of D-step loops on one lane.
             constexpr int SEGS = kWave / D, RP = NW * SEGS, NP = (D + RP - 1) / RP;
             const int jc = lane % D, seg = lane / D;
+            const int r0 = wave * SEGS + seg;   // this lane's row in pass 0
+            using Walk = RowWalk<D, TF, RP>;
+            const int wbase = Walk::base(r0, jc), wstep = Walk::step(jc), wtail = Walk::tail(jc);
+            const int tbase = rec_pos_theta<D, TF>(r0 < D ? r0 : 0);
+            auto pos_S = [&](int ps, int i) {
+                if constexpr (Walk::kLinear) return ps == 0 && r0 == 0 && jc >= G ? wtail : wbase + ps * wstep;
+                else return rec_pos_S<D, TF>(i, jc);
+            };
             // f_j = sum_{i<=j} S_ij xp_i: this lane's rows, then the other
             // segments of the wavefront, then the other wavefronts
             float fj = 0.0f;
 #pragma unroll
             for (int ps = 0; ps < NP; ++ps) {
-                const int i = ps * RP + wave * SEGS + seg;
-                if (i < D && i <= jc) fj = fmaf(s_old[rec_pos_S<D, TF>(i, jc)], s_xp[i], fj);
+                const int i = ps * RP + r0;
+                if (i < D && i <= jc) fj = fmaf(s_old[pos_S(ps, i)], s_xp[i], fj);
             }
             fj = segment_colsum<D>(fj);
             if constexpr (NW > 1) {
@@ -899,19 +949,22 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
             const float err = r - pred;
             // row i of S' = S M:  S'_ij = ca_j S_ij - cb_j g_ij with g_ij the
             // exclusive prefix sum of f_q S_iq along the row; its total is
-            // (S f)_i, so the gain is that total / alpha_{d-1}
+            // (S f)_i, so the gain is that total / alpha_{d-1} (one reciprocal
+            // for all rows: theta carries a 1e-3 tolerance, orders of
+            // magnitude above the ulp this gives away)
+            const float inv_al = 1.0f / al_last;
 #pragma unroll
             for (int ps = 0; ps < NP; ++ps) {
-                const int i = ps * RP + wave * SEGS + seg;
+                const int i = ps * RP + r0;
                 const bool in_row = i < D && i <= jc;
-                const int pos = rec_pos_S<D, TF>(i < D ? i : 0, jc);
+                const int pos = pos_S(ps, i < D ? i : 0);
                 const float sij = in_row ? s_old[pos] : 0.0f;
                 const float q = fj * sij;
                 const float qi = segment_scan<D>(q, lane);
                 if (in_row) s_new[pos] = ca * sij - cb * (qi - q);
                 if (i < D && jc == D - 1) {
-                    const int tp = rec_pos_theta<D, TF>(i);
-                    s_new[tp] = fmaf(qi / al_last, err, s_old[tp]);
+                    const int tp = tbase + ps * TF * (RP / 2);
+                    s_new[tp] = fmaf(qi * inv_al, err, s_old[tp]);
                 }
             }
             // padded tails: the fourth float of each lane slice's tail stays 0
