@@ -544,10 +544,12 @@ __device__ __forceinline__ float segment_colsum(float v) {
     return v;
 }
 
-// Workgroup-wide reductions through one LDS slot per wavefront.
+// Workgroup-wide reductions through one LDS slot per wavefront (a
+// one-wavefront workgroup needs neither the slots nor the barriers).
 template <class T, class Op>
 __device__ T block_reduce(T v, T *red, int lane, int wave, int nwave, Op op) {
     v = wave_reduce(v, op);
+    if (nwave == 1) return v;
     if (lane == 0) red[wave] = v;
     __syncthreads();
     T out = red[0];
@@ -1239,22 +1241,29 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
             s_top[wave][1] = top2;
         }
     }
-    if (lane == 0) {
-        s_red_v[wave] = b.v;
-        s_red_k[wave] = b.k;
-        s_red_n[wave] = n;
-        s_red_v2[wave] = sb.v;
-        s_red_k2[wave] = sb.k;
+    // a one-wavefront workgroup has its results in every lane already
+    if constexpr (NW > 1) {
+        if (lane == 0) {
+            s_red_v[wave] = b.v;
+            s_red_k[wave] = b.k;
+            s_red_n[wave] = n;
+            s_red_v2[wave] = sb.v;
+            s_red_k2[wave] = sb.k;
+        }
+        __syncthreads();
     }
-    __syncthreads();
     if (wave == 0) {
         // every lane of wavefront 0 reduces the per-wave results, then the
         // lanes write the instance block (action, count, context) at once
-        BestPair best{s_red_v[0], s_red_k[0]};
-        int cnt = s_red_n[0];
-        for (int w = 1; w < nwave; ++w) {
-            best = better(best, BestPair{s_red_v[w], s_red_k[w]});
-            cnt += s_red_n[w];
+        BestPair best = b;
+        int cnt = n;
+        if constexpr (NW > 1) {
+            best = BestPair{s_red_v[0], s_red_k[0]};
+            cnt = s_red_n[0];
+            for (int w = 1; w < nwave; ++w) {
+                best = better(best, BestPair{s_red_v[w], s_red_k[w]});
+                cnt += s_red_n[w];
+            }
         }
         const int a = best.k == 0x7fffffff ? -1 : best.k;
         // refinement after the decision: a window of 2*half+1 arms around the
@@ -1262,8 +1271,11 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
         int anchor = -1;
         if (p.rf.now && a >= 0) {
             if (p.rf.stat) {
-                BestPair sbest{s_red_v2[0], s_red_k2[0]};
-                for (int w = 1; w < nwave; ++w) sbest = better(sbest, BestPair{s_red_v2[w], s_red_k2[w]});
+                BestPair sbest = sb;
+                if constexpr (NW > 1) {
+                    sbest = BestPair{s_red_v2[0], s_red_k2[0]};
+                    for (int w = 1; w < nwave; ++w) sbest = better(sbest, BestPair{s_red_v2[w], s_red_k2[w]});
+                }
                 anchor = sbest.k == 0x7fffffff ? -1 : sbest.k;
             } else {
                 anchor = a;
@@ -1287,7 +1299,11 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
         if (lane == kInstAprev) blk[kInstAprev] = a;
         if (lane == kInstKact) blk[kInstKact] = cnt;
         if (sc != nullptr && lane == kInstGap) {
-            float t1 = s_top[0][0], t2 = s_top[0][1];
+            float t1 = top1, t2 = top2;   // one wavefront: already merged in every lane
+            if constexpr (NW > 1) {
+                t1 = s_top[0][0];
+                t2 = s_top[0][1];
+            }
             for (int w = 1; w < nwave; ++w) {
                 t2 = fmaxf(fminf(t1, s_top[w][0]), fmaxf(t2, s_top[w][1]));
                 t1 = fmaxf(t1, s_top[w][0]);
