@@ -335,33 +335,53 @@ def copy_rate(dev, reps):
 CEILING_LIB = os.path.join(ROOT, "paper_2508_01744_amd", "libagft_ceiling.so")
 
 
-def stream_ceiling(wl, launches=20):
-    """The attainable rate of this workload's step traffic without its
+# workgroups per compute unit the stream ceiling is measured at (0: uncapped);
+# the rate of concurrent instance streams depends on how many run at once,
+# so the ceiling is the best of these
+CEILING_CAPS = (0, 6, 5, 4, 3)
+
+
+def stream_ceiling(wl, launches=20, caps=CEILING_CAPS):
+    """The attainable HBM rate of the step's memory traffic without its
     arithmetic (libagft_ceiling.so): one workgroup per instance reads every
     chunk of an instance-sized region of the step kernel's record layout,
     then, in the second form, writes one record back, as the step's update
-    does.  Returns both rates in GB/s (bytes moved over the average launch
-    duration) and the durations."""
+    does; each form at every cap on workgroups per compute unit in `caps`
+    that the device admits, the fastest kept.  Returns both rates in GB/s
+    (bytes moved over the average launch duration), the durations, the caps
+    they came from and every cap's durations."""
     import ctypes
     from paper_2508_01744_amd import launch_shape, workload_config
     if not os.path.exists(CEILING_LIB):
         raise RuntimeError(f"{CEILING_LIB} is not built: run __graft_entry__.build()")
     lib = ctypes.CDLL(CEILING_LIB)
-    lib.agft_stream_ceiling.restype = ctypes.c_int
-    lib.agft_stream_ceiling.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
-                                        ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    f = lib.agft_stream_ceiling_at
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
     tf = launch_shape(workload_config(wl))["tail_floats"]
     nb = 64 // wl.d
     rec = (wl.d // 2) * (wl.d // 4) + (wl.d // 2) * tf // 4      # 16-byte chunks per arm record
     chunks = -(-wl.K // nb) * nb * rec                           # per instance, blocks of nb arms
-    r_us, rw_us = ctypes.c_double(), ctypes.c_double()
-    code = lib.agft_stream_ceiling(wl.B, chunks, rec, launches, ctypes.byref(r_us), ctypes.byref(rw_us))
-    if code != 0:
-        raise RuntimeError(f"agft_stream_ceiling failed ({code})")
+    by_cap = {}
+    for cap in caps:
+        r_us, rw_us = ctypes.c_double(), ctypes.c_double()
+        code = f(wl.B, chunks, rec, launches, cap, ctypes.byref(r_us), ctypes.byref(rw_us))
+        if code == 3:      # the device's occupancy calculator does not confirm this cap
+            continue
+        if code != 0:
+            raise RuntimeError(f"agft_stream_ceiling_at failed ({code}) at {cap} workgroups per compute unit")
+        by_cap[cap] = {"read_us": r_us.value, "read_writeback_us": rw_us.value}
+    if not by_cap:
+        raise RuntimeError("agft_stream_ceiling_at admitted none of the caps")
+    cap_r = min(by_cap, key=lambda c: by_cap[c]["read_us"])
+    cap_rw = min(by_cap, key=lambda c: by_cap[c]["read_writeback_us"])
+    r_us, rw_us = by_cap[cap_r]["read_us"], by_cap[cap_rw]["read_writeback_us"]
     read_b, write_b = wl.B * chunks * 16, wl.B * rec * 16
-    return {"read_gbs": read_b / (r_us.value * 1e-6) / 1e9,
-            "read_writeback_gbs": (read_b + write_b) / (rw_us.value * 1e-6) / 1e9,
-            "read_us": r_us.value, "read_writeback_us": rw_us.value,
+    return {"read_gbs": read_b / (r_us * 1e-6) / 1e9,
+            "read_writeback_gbs": (read_b + write_b) / (rw_us * 1e-6) / 1e9,
+            "read_us": r_us, "read_writeback_us": rw_us, "read_cap": cap_r, "read_writeback_cap": cap_rw,
+            "by_cap": {str(c): v for c, v in by_cap.items()},
             "bytes_per_launch": read_b, "writeback_bytes_per_launch": write_b, "launches": launches}
 
 
@@ -458,14 +478,17 @@ def main():
         res["roofline"]["ceiling"] = {
             "read_gbs": max(c0["read_gbs"], c1["read_gbs"]), "read_writeback_gbs": rw,
             "achieved_over_read_writeback": head["achieved_gbs"] / rw,
-            "after_headline": {"read_gbs": c0["read_gbs"], "read_writeback_gbs": c0["read_writeback_gbs"]},
-            "after_idle": {"read_gbs": c1["read_gbs"], "read_writeback_gbs": c1["read_writeback_gbs"]},
+            "after_headline": {k: c0[k] for k in ("read_gbs", "read_writeback_gbs", "read_cap",
+                                                   "read_writeback_cap", "by_cap")},
+            "after_idle": {k: c1[k] for k in ("read_gbs", "read_writeback_gbs", "read_cap",
+                                              "read_writeback_cap", "by_cap")},
             "what": (f"the step's traffic without its arithmetic on {wl.name}'s record layout "
                      f"({c0['bytes_per_launch'] / wl.B:.0f} B read per instance, one "
                      f"{c0['writeback_bytes_per_launch'] / wl.B:.0f} B record written back), one workgroup "
-                     f"per instance, non-temporal loads and stores; average of {c0['launches']} launches, "
-                     f"measured right after the headline run and again after 1 s of idle, the faster "
-                     f"of the two reported")}
+                     f"per instance, non-temporal loads and stores; average of {c0['launches']} launches "
+                     f"at each cap on workgroups per compute unit in {list(CEILING_CAPS)} (0: none; "
+                     f"durations in us by cap), the fastest kept; measured right after the headline run "
+                     f"and again after 1 s of idle, the faster of the two reported")}
     if not args.no_workloads:
         runs = {}
         for name in DETAIL_WORKLOADS:

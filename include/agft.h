@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define AGFT_ABI_VERSION 5
+#define AGFT_ABI_VERSION 6
 
 enum agft_status {
     AGFT_OK = 0,
@@ -236,12 +236,13 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
               float *d_scores);
 
 /* How agft_step launches the step kernel for cfg (host-only, no device
- * call): one workgroup per instance.  The four fields follow from the
+ * call): one workgroup per instance.  The five fields follow from the
  * configuration alone: the bytes an exploring instance streams per step
  * (arms in play times 4(d + d(d+1)/2)) choose the record layout, with the
  * switch the bytes an exploiting instance streams choose the workgroup
- * width, and d, the layout and the pruning rules choose the register target
- * and where the update runs. */
+ * width, d, the layout and the pruning rules choose the register target
+ * and where the update runs, and the width with the register target the
+ * cap on workgroups per compute unit. */
 typedef struct agft_launch_shape {
     int32_t waves;        /* wavefronts per workgroup: 1 up to 16 KB streamed per
                              instance, 4 beyond */
@@ -249,6 +250,9 @@ typedef struct agft_launch_shape {
     int32_t tail_floats;  /* record layout, as agft_state_view.tail_floats */
     int32_t early_update; /* 1: the rank-1 update runs while the stream's first pass
                              is in flight; 0: after the stream */
+    int32_t cu_workgroups;  /* workgroups per compute unit agft_step's launch admits
+                               (its LDS request caps them there); 0: no cap.
+                               agft_sim_step launches uncapped. */
 } agft_launch_shape;
 
 /* Fill *out for cfg.  AGFT_E_INVAL if cfg is invalid or out is NULL,

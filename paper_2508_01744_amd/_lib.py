@@ -52,10 +52,11 @@ class agft_env_config(ctypes.Structure):
 
 
 class agft_launch_shape(ctypes.Structure):
-    _fields_ = [("waves", _i32), ("simd_waves", _i32), ("tail_floats", _i32), ("early_update", _i32)]
+    _fields_ = [("waves", _i32), ("simd_waves", _i32), ("tail_floats", _i32), ("early_update", _i32),
+                ("cu_workgroups", _i32)]
 
 
-ABI_VERSION = 5   # AGFT_ABI_VERSION of the agft_config layout declared here
+ABI_VERSION = 6   # AGFT_ABI_VERSION of the agft_config layout declared here
 
 EXPORTED = ["agft_state_bytes", "agft_create", "agft_step", "agft_get_state", "agft_export",
             "agft_set_stream", "agft_destroy", "agft_strerror", "agft_abi_version", "agft_launch_shape_for",

@@ -1,19 +1,22 @@
 // agft_step.hip -- batched AGFT decide-and-update step for CDNA4 (gfx950).
 //
 // One workgroup per tuner instance.  Each arm's record (theta_k and the
-// packed upper factor S_k of A_k^{-1}) is contiguous in HBM and is read by a
-// group of G = d/2 lanes: lane j of the group owns factor columns j and
-// d-1-j (d+1 elements together) and theta_{2j}, theta_{2j+1}, so it forms
-// two complete entries of v = S^T x_t and two terms of theta^T x_t on its
-// own, and the group only sums two numbers at the end.  For every load
-// instruction the G lanes of a group read G x 16 contiguous bytes of one
-// record and a wavefront covers whole cache lines.  Keeping a record
-// contiguous matters for the update: rewriting one arm touches a handful of
-// cache lines instead of one line per 16-byte piece.
+// packed upper factor S_k of A_k^{-1}) is read by a group of G = d/2 lanes:
+// lane j of the group owns factor columns j and d-1-j (d+1 elements
+// together) and theta_{2j}, theta_{2j+1}, so it forms two complete entries
+// of v = S^T x_t and two terms of theta^T x_t on its own, and the group only
+// sums two numbers at the end.  A record's main part is contiguous in HBM
+// and its short tail sits beside the tails of the other arms of its block
+// (Rec below): for every load instruction the G lanes of a group read G x 16
+// contiguous bytes of one record and a wavefront covers whole cache lines,
+// and rewriting one arm touches a handful of cache lines instead of one line
+// per 16-byte piece.
 //
 // Per step and instance (Sec. 4.2-4.4):
-//   0. with the switch to exploitation on, feed the previous reward to the
-//      instance's Page-Hinkley test and switch when the rewards are stable;
+//   0. read the instance's words, mask, context and reward, all in one
+//      memory round trip; with the switch to exploitation on, feed the
+//      previous reward to the instance's Page-Hinkley test and switch when
+//      the rewards are stable;
 //   1. fetch the record of the previous decision's arm (its update waits);
 //      with the paper's pruning rules on, drop arms by their reward counts
 //      and means; list the other arms in play (in the action space, not
@@ -45,6 +48,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -323,7 +327,9 @@ int waves_for(const agft_config &c) {
 // Whether the update of the previous decision's arm runs before the stream
 // (its first pass lands meanwhile and the chain gets shorter) rather than
 // after it: always, except at d = 32 where an instance streams more than
-// 16 KB, since there the longer update holds back the second pass.
+// 16 KB, since there the longer update holds back the second pass (the
+// kernel still runs it before the stream at a step whose list of arms fits
+// in one pass).
 // Measured on MI355X (step kernel, before / after the stream): K=64 d=8
 // B=4,096 19.1 / 20.5 us; K=128 d=16 B=65,536 853 / 857 us, B=16,384 218.4 /
 // 220.8 us; K=256 d=32 B=1,024 92.4 / 91.7 us.
@@ -573,6 +579,20 @@ int occupancy_for(const agft_config &c, int tail) {
     return c.d == 16 && tail == 3 && !(c.prune_rule & 14) ? 6 : 7;
 }
 
+// Workgroups per compute unit for four-wavefront workgroups at six
+// wavefronts per SIMD (d = 16, packed tails, no rules 2-8): 4, enforced by
+// the launch's LDS request.  There the chain of phases per instance is short
+// beside its stream, and four instances per compute unit keep enough of the
+// stream in flight to hold the HBM rate, while more interleave more
+// concurrent streams and lose rate.  Measured on MI355X (step kernel, us, at
+// 6 / 5 / 4 / 3 workgroups per compute unit): K=128 d=16 B=65,536 823.6 /
+// 819.5 / 807.8 / 858.0, B=16,384 199.0 / 197.5 / 197.1 / 209.4.  Not with
+// the paper's rules 2-8, whose pass over the arm statistics needs the
+// instances in flight (K=128 d=16 B=65,536: 827.7 uncapped, 852.6 at 5,
+// 911.1 at 4), nor for one-wavefront workgroups, whose steps are short
+// chains with little to stream.
+int cu_workgroups_for(int waves, int simd_waves) { return waves == 4 && simd_waves == 6 ? 4 : 0; }
+
 // ENV: the simulator's environment responds in the epilogue (agft_sim_step):
 // once the decision is known, the first lanes of wavefront 0 run the
 // instance's next window with it, writing the reward and the next context in
@@ -626,41 +646,66 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
     __shared__ int2 s_stu;      // its arm's reward count and sum
 
     const bool decide = p.ctx != nullptr;
-    // the instance's mask words, issued first: they depend on nothing, and the
-    // list of arms to stream waits for them
-    const uint32_t raw_word = (wave == 0 && lane < KW) ? p.mask[(size_t)inst * KW + lane] : 0u;
-
-    // Per-instance words, uniform over the workgroup (scalar loads at kernel
-    // start): context, previous decision and its reward.  The previous
-    // decision's context is only needed by the update after the stream, so it
-    // waits in LDS rather than in scalar registers.
+    int32_t *blk = p.inst + (size_t)inst * p.IW;
+    // Everything the step reads before it knows the previous decision's arm is
+    // requested at once, so that the prologue waits for one memory round trip
+    // rather than one per item (the vector loads first: the compiler's waits
+    // for the addresses of later ones would hold them back behind the scalar
+    // loads).  Vector loads, by wavefront 0: the environment's state of the
+    // instance (for the epilogue), the instance's mask words and the previous
+    // decision's context; at D = 32 also the context, by every wavefront.
+    // Scalar loads: the instance's first sixteen words, the reward and, up
+    // to D = 16, the context.
+    __shared__ uint32_t s_envw[ENV ? 32 : 1];
+    uint32_t env_pre = 0u;
+    if constexpr (ENV)
+        if (wave == 0) env_pre = agft_env_detail::env_prefetch(env, inst, lane);
+    const int lane_d = lane < D ? lane : 0;   // clamped element index
+    const uint32_t *mask_at = p.mask + (size_t)inst * KW + (lane < KW ? lane : 0);
+    const float *xp_at = reinterpret_cast<const float *>(blk + kInstX) + lane_d;
+    uint32_t raw_word = 0u;
+    float xp_word = 0.0f;
+    if (wave == 0) {
+        raw_word = *mask_at;
+        xp_word = *xp_at;
+    }
+    const int4 *blk4 = reinterpret_cast<const int4 *>(blk);
+    const int4 wa = blk4[0], wb = blk4[1], wc = blk4[2], wd = blk4[3];
+    // (no branch around the reward either: without a pending decision the
+    // block's first word stands in for it, unused)
+    const float r_in = *(p.apply_update ? p.reward + inst : reinterpret_cast<const float *>(blk));
+    // The context, without a branch: a flush reads the block's own words in
+    // its place, and nothing uses them (x_ok is false, so no arm is listed,
+    // scored or stashed).  Non-finite test on the exponent bits (both
+    // operands of the and evaluated: a short-circuit branch would hold back
+    // the loads after it).  Up to D = 16 the context comes by scalar loads;
+    // at D = 32 lane l < D reads element l and the selectors below take the
+    // values from the lanes, so that 32 scalar registers are not held while
+    // the loads are in flight (they would push the scalar loads apart).
+    const float *xi = decide ? p.ctx + (size_t)inst * D : reinterpret_cast<const float *>(blk);
     float x[D];
-    bool x_ok = decide;
-    if (decide) {
-        const float *xi = p.ctx + (size_t)inst * D;
-        // non-finite test on the exponent bits, in scalar integer arithmetic
+    float x_lane;   // element `lane` of the context, lanes < D
+    bool x_ok;
+    if constexpr (D <= 16) {
         uint32_t nonfinite = 0u;
 #pragma unroll
         for (int q = 0; q < D; ++q) {
             x[q] = xi[q];
             nonfinite |= (__float_as_uint(x[q]) & 0x7f800000u) == 0x7f800000u ? 1u : 0u;
         }
-        x_ok = nonfinite == 0u;
+        x_ok = decide & (nonfinite == 0u);
+        x_lane = pick<D>(x, lane);
     } else {
+        x_lane = xi[lane_d];
+        x_ok = decide & (__ballot((__float_as_uint(x_lane) & 0x7f800000u) == 0x7f800000u) == 0ull);
 #pragma unroll
-        for (int q = 0; q < D; ++q) x[q] = 0.0f;
+        for (int q = 0; q < D; ++q) x[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x_lane), q));
     }
+
     // The context also waits in LDS for its later readers (the exploiting
-    // stream and the stash in the epilogue), so that its D scalar registers
-    // die once this lane's selectors below are formed: held through the step
-    // at D = 32 they would push the scalar registers into spills.
+    // stream and the stash in the epilogue).
     __shared__ float s_x[D];
-    if (wave == 0 && lane < D) s_x[lane] = decide ? p.ctx[(size_t)inst * D + lane] : 0.0f;
-    // the environment's state of this instance, fetched now for the epilogue
-    __shared__ uint32_t s_envw[ENV ? 32 : 1];
-    uint32_t env_pre = 0u;
-    if constexpr (ENV)
-        if (wave == 0) env_pre = agft_env_detail::env_prefetch(env, inst, lane);
+    if (wave == 0 && lane < D) s_x[lane] = x_lane;
     // This lane's selectors of x: xa_e = x_e for e <= j, xb_e = x_{D-e} for e > j.
     float xa[D + 1], xb[D + 1];
 #pragma unroll
@@ -669,25 +714,31 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
         xb[e] = (e > j && e >= 1) ? x[D - e < 0 ? 0 : D - e] : 0.0f;
     }
     const float xt0 = pick<D>(x, 2 * j), xt1 = pick<D>(x, 2 * j + 1);
-    int32_t *blk = p.inst + (size_t)inst * p.IW;
-    const int a_prev = p.apply_update ? blk[kInstAprev] : -1;
+    const int a_prev = p.apply_update ? wa.x : -1;   // word kInstAprev
     const bool has_prev = a_prev >= 0 && a_prev < K;
-    const float r = has_prev ? p.reward[inst] : 0.0f;
+    // (taken back to a scalar register: the select leaves it in a vector one)
+    const float r = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(has_prev ? r_in : 0.0f)));
     const bool upd = has_prev && isfinite(r);
     const int a_upd = upd ? a_prev : -1;
-    if (upd && wave == 0 && lane < D) s_xp[lane] = reinterpret_cast<const float *>(blk + kInstX)[lane];
 
     // Page-Hinkley test on the instance's rewards and the switch to greedy
     // exploitation (uniform scalar code, single precision, fixed order).
-    int mode = p.e.on ? blk[kInstMode] : -1;
+    static_assert(kInstMode == 3 && kInstPh == 4 && kInstPhLast == 10 && kInstPhMargin == 11 && kInstLo == 12 &&
+                      kInstHi == 13 && kInstStride == 14,
+                  "word order of the instance block");
+    int mode = p.e.on ? wa.w : -1;
     float ph[6] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     int ph_last = 0;
     float ph_margin = 0.0f;
     if (p.e.on) {
-#pragma unroll
-        for (int q = 0; q < 6; ++q) ph[q] = __int_as_float(blk[kInstPh + q]);
-        ph_last = blk[kInstPhLast];
-        ph_margin = __int_as_float(blk[kInstPhMargin]);
+        ph[0] = __int_as_float(wb.x);
+        ph[1] = __int_as_float(wb.y);
+        ph[2] = __int_as_float(wb.z);
+        ph[3] = __int_as_float(wb.w);
+        ph[4] = __int_as_float(wc.x);
+        ph[5] = __int_as_float(wc.y);
+        ph_last = wc.z;
+        ph_margin = __int_as_float(wc.w);
         if (upd && mode < 0) {
             ph[0] = ph[0] + 1.0f;
             ph[1] = ph[1] + (r - ph[1]) / ph[0];
@@ -717,9 +768,21 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
                                : tid == kInstPhMargin ? __float_as_int(ph_margin)
                                : __float_as_int(pick<6>(ph, tid - kInstPh));
 
-    // Record of the previous decision's arm: fetched now, staged in LDS before the stream.
-    // Its reward count and sum are fetched with it, so that the end of the
-    // step only stores them.
+    // the arms in play: not removed by a pruning rule, inside the action space;
+    // at a rule-1 step of the non-sticky reading, every arm of the space
+    const int sp_lo = wd.x, sp_hi = wd.y;
+    const int sp_st = wd.z > 1 ? wd.z : 1;
+    const bool reset = p.prune_reset && !greedy && x_ok;
+    if (wave == 0 && lane < KW) {
+        s_raw[lane] = raw_word;
+        s_mask[lane] = (reset ? 0xffffffffu : raw_word) & space_bits(lane, sp_lo, sp_hi, sp_st);
+    }
+    if (upd && wave == 0 && lane < D) s_xp[lane] = xp_word;
+
+    // Record of the previous decision's arm, requested once its index is
+    // known (after the LDS stores above, which would otherwise wait for it
+    // too) and staged in LDS before the stream.  Its reward count and sum
+    // are fetched with it, so that the end of the step only stores them.
     float4 old_chunk[NQ];
     int2 st_upd = make_int2(0, 0);
     if (upd) {
@@ -729,16 +792,6 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
             if (c < R::R) old_chunk[q] = ld_record<D>(recs + rec_chunk(D, TF, a_upd, c));
         }
         if (p.keep_stats && tid == 0) st_upd = p.stats[(size_t)inst * K + a_upd];
-    }
-
-    // the arms in play: not removed by a pruning rule, inside the action space;
-    // at a rule-1 step of the non-sticky reading, every arm of the space
-    const int sp_lo = blk[kInstLo], sp_hi = blk[kInstHi];
-    const int sp_st = blk[kInstStride] > 1 ? blk[kInstStride] : 1;
-    const bool reset = p.prune_reset && !greedy && x_ok;
-    if (wave == 0 && lane < KW) {
-        s_raw[lane] = raw_word;
-        s_mask[lane] = (reset ? 0xffffffffu : raw_word) & space_bits(lane, sp_lo, sp_hi, sp_st);
     }
 
     // The paper's pruning rules (Sec. 4.3) on the arms active at step start,
@@ -904,8 +957,9 @@ void agft_step_kernel(StepArgs p, agft_env_detail::EnvArgs env) {
 
     // ---- square-root rank-1 update of the previous decision's arm ----
     // Run while the stream's first pass is in flight, or after the stream
-    // (early_update on the host decides which), in LDS; the updated record
-    // is written back as the kernel's last act (write_back below).
+    // (early_update on the host decides which, and the kernel runs it early
+    // whenever the whole list fits in the first pass), in LDS; the updated
+    // record is written back as the kernel's last act (write_back below).
     auto update = [&]() {
         if (upd) {
             // Lane l of every wavefront takes column j = l % D of one row per
@@ -1495,13 +1549,66 @@ T *at(char *base, size_t off) {
 
 // The step kernel for one or four wavefronts per workgroup (the two widths
 // waves_for chooses), each compiled for its width.
+// Dynamic LDS that caps a kernel at `cap` workgroups per compute unit: a
+// 1/cap share of the unit's LDS less the kernel's static LDS, lowered in
+// 512-byte steps until the occupancy calculator admits exactly cap
+// workgroups (allocation granules round a request up).  Worked out once per
+// kernel and device; a share the calculator does not confirm, or below what
+// the kernel needs, leaves the launch uncapped.  Only host queries, no
+// allocation; a failed query is cleared so that the launch's own error check
+// does not see it.
+constexpr int kMaxDevices = 64;
+template <int D, int TF, int W, int NW, bool ENV>
+std::atomic<int64_t> *capped_lds_cache() {
+    static std::atomic<int64_t> cache[kMaxDevices];   // 0: not worked out; else bytes + 1
+    return cache;
+}
+
+size_t capped_lds(const void *kernel, int threads, size_t need, int cap, std::atomic<int64_t> *cache) {
+    if (cap <= 0) return need;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        (void)hipGetLastError();
+        return need;
+    }
+    int64_t v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        int64_t dyn = 0;   // 0: uncapped
+        int per_cu = 0;
+        hipFuncAttributes fa;
+        if (hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
+            hipFuncGetAttributes(&fa, kernel) == hipSuccess && per_cu > 0) {
+            const int64_t max_dyn = 64 * 1024 - (int64_t)fa.sharedSizeBytes;
+            for (int64_t d = (per_cu / cap - (int64_t)fa.sharedSizeBytes) / 16 * 16;
+                 d >= (int64_t)need && d > 0; d -= 512) {
+                int blocks = 0;
+                if (d > max_dyn) continue;
+                if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, threads, (size_t)d) != hipSuccess)
+                    break;
+                if (blocks == cap) {
+                    dyn = d;
+                    break;
+                }
+                if (blocks > cap) break;
+            }
+        }
+        (void)hipGetLastError();
+        v = dyn + 1;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v > 1 ? (size_t)(v - 1) : need;
+}
+
 template <int D, int TF, int W, bool ENV>
-void launch_width(int waves, unsigned grid, size_t lds, hipStream_t stream, const StepArgs &p,
+void launch_width(int waves, int cap, unsigned grid, size_t lds, hipStream_t stream, const StepArgs &p,
                   const agft_env_detail::EnvArgs &e) {
-    if (waves == 1)
+    if (waves == 1) {
         hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 1, ENV>), dim3(grid), dim3(kWave), lds, stream, p, e);
-    else
+    } else {
+        lds = capped_lds(reinterpret_cast<const void *>(&agft_step_kernel<D, TF, W, 4, ENV>), 4 * kWave, lds, cap,
+                         capped_lds_cache<D, TF, W, 4, ENV>());
         hipLaunchKernelGGL((agft_step_kernel<D, TF, W, 4, ENV>), dim3(grid), dim3(4 * kWave), lds, stream, p, e);
+    }
 }
 
 // One decision for every instance of handle h (and, with env, the
@@ -1561,9 +1668,14 @@ int launch_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32
     hipStream_t s = h->stream;
     agft_env_detail::EnvArgs e{};
     if (env != nullptr) e = *env;
-#define AGFT_LAUNCH(D_, TF_, W_)                                                  \
-    (env != nullptr ? launch_width<D_, TF_, W_, true>(waves, grid, lds, s, p, e) \
-                    : launch_width<D_, TF_, W_, false>(waves, grid, lds, s, p, e))
+    // The simulator's step launches uncapped: the environment's response at
+    // the end of each workgroup wants more instances in flight (K=128 d=16,
+    // us per fused step, uncapped / at 4: B=65,536 881.5 / 891.0, B=16,384
+    // 211.9 / 218.0).
+    const int cap = env != nullptr ? 0 : shape.cu_workgroups;
+#define AGFT_LAUNCH(D_, TF_, W_)                                                       \
+    (env != nullptr ? launch_width<D_, TF_, W_, true>(waves, cap, grid, lds, s, p, e) \
+                    : launch_width<D_, TF_, W_, false>(waves, cap, grid, lds, s, p, e))
     switch (c.d) {
         case 8:
             if (packed_tails) AGFT_LAUNCH(8, 3, 7);
@@ -1708,6 +1820,7 @@ int agft_launch_shape_for(const agft_config *cfg, agft_launch_shape *out) {
     out->tail_floats = tail_floats(*cfg);
     out->simd_waves = occupancy_for(*cfg, out->tail_floats);
     out->early_update = early_update(*cfg) ? 1 : 0;
+    out->cu_workgroups = cu_workgroups_for(out->waves, out->simd_waves);
     return AGFT_OK;
 }
 

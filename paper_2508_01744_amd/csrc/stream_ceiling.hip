@@ -14,14 +14,21 @@
 // per-instance write-back adds to it.
 //
 // Built as its own library (libagft_ceiling.so), apart from the tuner's:
-//   int agft_stream_ceiling(int64_t instances, int64_t chunks, int32_t record_chunks,
-//                           int32_t launches, double *read_us, double *read_writeback_us)
+//   int agft_stream_ceiling_at(int64_t instances, int64_t chunks, int32_t record_chunks,
+//                              int32_t launches, int32_t cu_workgroups,
+//                              double *read_us, double *read_writeback_us)
 // allocates a zero-filled buffer of instances x chunks x 16 bytes on the
 // current device, times each form over `launches` launches on the null
 // stream (after two untimed ones), writes the average duration of each in
-// microseconds and frees the buffer.  Returns 0; 1 for arguments out of range
-// (instances and chunks in [1, 2^31), record_chunks in [1, 256] and <= chunks,
-// launches >= 1); 2 for a HIP error (reported on stderr).
+// microseconds and frees the buffer.  cu_workgroups > 0 caps the workgroups
+// per compute unit by the launches' LDS request (a 1/cap share of the unit's
+// LDS, confirmed by the occupancy calculator), since the rate of concurrent
+// streams depends on how many run at once; 0 leaves them uncapped.
+// agft_stream_ceiling(...) without cu_workgroups is the uncapped form.
+// Returns 0; 1 for arguments out of range (instances and chunks in [1, 2^31),
+// record_chunks in [1, 256] and <= chunks, launches >= 1, cu_workgroups in
+// [0, 64]); 2 for a HIP error (reported on stderr); 3 for a cap the
+// occupancy calculator does not confirm.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -73,13 +80,41 @@ bool ok(hipError_t e, const char *what) {
     return false;
 }
 
+// Dynamic LDS per workgroup that admits exactly `cap` workgroups of the
+// kernel per compute unit (0 when cap is 0); -1 if none does.
+int64_t cap_lds(const void *kernel, int cap) {
+    if (cap == 0) return 0;
+    int dev = 0, per_cu = 0;
+    hipFuncAttributes fa;
+    if (!ok(hipGetDevice(&dev), "hipGetDevice") ||
+        !ok(hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev), "attribute") ||
+        !ok(hipFuncGetAttributes(&fa, kernel), "hipFuncGetAttributes"))
+        return -2;
+    const int64_t max_dyn = 64 * 1024 - (int64_t)fa.sharedSizeBytes;
+    for (int64_t d = ((int64_t)per_cu / cap - (int64_t)fa.sharedSizeBytes) / 16 * 16; d > 0; d -= 512) {
+        if (d > max_dyn) continue;
+        int blocks = 0;
+        if (!ok(hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, kThreads, (size_t)d), "occupancy"))
+            return -2;
+        if (blocks == cap) return d;
+        if (blocks > cap) break;
+    }
+    return -1;
+}
+
 }  // namespace
 
-extern "C" int agft_stream_ceiling(int64_t inst, int64_t chunks, int32_t rec, int32_t launches, double *read_us,
-                                   double *read_writeback_us) {
-    if (inst < 1 || inst > 0x7fffffffL || chunks < 1 || chunks > 0x7fffffffL || rec < 1 || rec > kThreads || rec > chunks || launches < 1 ||
-        read_us == nullptr || read_writeback_us == nullptr)
+extern "C" int agft_stream_ceiling_at(int64_t inst, int64_t chunks, int32_t rec, int32_t launches,
+                                      int32_t cu_workgroups, double *read_us, double *read_writeback_us) {
+    if (inst < 1 || inst > 0x7fffffffL || chunks < 1 || chunks > 0x7fffffffL || rec < 1 || rec > kThreads ||
+        rec > chunks || launches < 1 || cu_workgroups < 0 || cu_workgroups > 64 || read_us == nullptr ||
+        read_writeback_us == nullptr)
         return 1;
+    int64_t lds[2];
+    lds[0] = cap_lds(reinterpret_cast<const void *>(&stream_kernel<false>), cu_workgroups);
+    lds[1] = cap_lds(reinterpret_cast<const void *>(&stream_kernel<true>), cu_workgroups);
+    if (lds[0] == -2 || lds[1] == -2) return 2;
+    if (lds[0] < 0 || lds[1] < 0) return 3;
     const size_t bytes = (size_t)inst * (size_t)chunks * 16;
     f4 *buf = nullptr;
     float *sink = nullptr;
@@ -93,11 +128,11 @@ extern "C" int agft_stream_ceiling(int64_t inst, int64_t chunks, int32_t rec, in
     for (int form = 0; form < 2 && rc == 0; ++form) {
         auto launch = [&]() {
             if (form == 0)
-                hipLaunchKernelGGL(stream_kernel<false>, dim3((unsigned)inst), dim3(kThreads), 0, 0, buf, (int)chunks,
-                                   (int)rec, sink);
+                hipLaunchKernelGGL(stream_kernel<false>, dim3((unsigned)inst), dim3(kThreads), (size_t)lds[0], 0, buf,
+                                   (int)chunks, (int)rec, sink);
             else
-                hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)inst), dim3(kThreads), 0, 0, buf, (int)chunks,
-                                   (int)rec, sink);
+                hipLaunchKernelGGL(stream_kernel<true>, dim3((unsigned)inst), dim3(kThreads), (size_t)lds[1], 0, buf,
+                                   (int)chunks, (int)rec, sink);
         };
         launch();
         launch();
@@ -119,4 +154,9 @@ extern "C" int agft_stream_ceiling(int64_t inst, int64_t chunks, int32_t rec, in
     if (buf != nullptr) (void)hipFree(buf);
     if (sink != nullptr) (void)hipFree(sink);
     return rc;
+}
+
+extern "C" int agft_stream_ceiling(int64_t inst, int64_t chunks, int32_t rec, int32_t launches, double *read_us,
+                                   double *read_writeback_us) {
+    return agft_stream_ceiling_at(inst, chunks, rec, launches, 0, read_us, read_writeback_us);
 }

@@ -44,7 +44,7 @@ def workload_config(wl, B=None):
 
 def launch_shape(cfg):
     """How agft_step launches the step kernel for cfg: dict(waves,
-    simd_waves, tail_floats, early_update)."""
+    simd_waves, tail_floats, early_update, cu_workgroups)."""
     code, shape = L.agft_launch_shape_for(cfg)
     L.check("agft_launch_shape_for", code)
     return {name: int(getattr(shape, name)) for name, _ in shape._fields_}

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert L.agft_abi_version() == L.ABI_VERSION == 5
+    assert L.agft_abi_version() == L.ABI_VERSION == 6
     for code in (0, -1, -2, -3, -4):
         assert L.agft_strerror(code)
     assert L.agft_strerror(-99) == "unknown status"

@@ -33,16 +33,23 @@ def test_step_kernels_do_not_spill(tmp_path):
 
 def test_stream_ceiling_library_checks_its_arguments():
     """The bench's ceiling library is built beside the tuner's, exports its
-    one entry point and rejects out-of-range arguments before any HIP call."""
+    two entry points and rejects out-of-range arguments before any HIP call."""
     import ctypes
     assert os.path.exists(_build.CEILING_LIB), "run __graft_entry__.build()"
     lib = ctypes.CDLL(_build.CEILING_LIB)
+    dp = ctypes.POINTER(ctypes.c_double)
     f = lib.agft_stream_ceiling
     f.restype = ctypes.c_int
-    f.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
-                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]
+    f.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, dp, dp]
+    g = lib.agft_stream_ceiling_at
+    g.restype = ctypes.c_int
+    g.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, dp, dp]
     a, b = ctypes.c_double(), ctypes.c_double()
     for args in ((0, 4864, 38, 1), (1 << 31, 4864, 38, 1), (1, 0, 1, 1), (1, 4864, 0, 1), (1, 4864, 257, 1),
                  (1, 10, 38, 1), (1, 4864, 38, 0)):
         assert f(*args, ctypes.byref(a), ctypes.byref(b)) == 1, args
+        assert g(*args, 0, ctypes.byref(a), ctypes.byref(b)) == 1, args
     assert f(1, 4864, 38, 1, None, ctypes.byref(b)) == 1
+    assert g(1, 4864, 38, 1, -1, ctypes.byref(a), ctypes.byref(b)) == 1
+    assert g(1, 4864, 38, 1, 65, ctypes.byref(a), ctypes.byref(b)) == 1
+    assert g(1, 4864, 38, 1, 4, ctypes.byref(a), None) == 1

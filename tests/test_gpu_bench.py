@@ -53,6 +53,11 @@ def test_bench_json_line():
     for when in ("after_headline", "after_idle"):
         assert 0 < ce[when]["read_writeback_gbs"] <= ce["read_writeback_gbs"]
         assert 0 < ce[when]["read_gbs"] <= ce["read_gbs"]
+        # every cap the device admits was timed, the fastest kept
+        by_cap = ce[when]["by_cap"]
+        assert "0" in by_cap and set(by_cap) <= {"0", "6", "5", "4", "3"}
+        assert by_cap[str(ce[when]["read_writeback_cap"])]["read_writeback_us"] == \
+            min(v["read_writeback_us"] for v in by_cap.values())
     # every workload over its whole horizon beside the headline
     wls = det["workloads"]
     assert set(wls) == {"cfg1", "cfg2", "cfg3", "cfg4", "cfg5"}
