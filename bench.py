@@ -341,13 +341,14 @@ CEILING_LIB = os.path.join(ROOT, "paper_2508_01744_amd", "libagft_ceiling.so")
 CEILING_CAPS = (0, 6, 5, 4, 3)
 
 
-def stream_ceiling(wl, launches=20, caps=CEILING_CAPS):
+def stream_ceiling(wl, launches=20, caps=CEILING_CAPS, rest_s=0.0):
     """The attainable HBM rate of the step's memory traffic without its
     arithmetic (libagft_ceiling.so): one workgroup per instance reads every
     chunk of an instance-sized region of the step kernel's record layout,
     then, in the second form, writes one record back, as the step's update
     does; each form at every cap on workgroups per compute unit in `caps`
-    that the device admits, the fastest kept.  Returns both rates in GB/s
+    that the device admits (after `rest_s` seconds of idle before each
+    cap), the fastest kept.  Returns both rates in GB/s
     (bytes moved over the average launch duration), the durations, the caps
     they came from and every cap's durations."""
     import ctypes
@@ -365,6 +366,8 @@ def stream_ceiling(wl, launches=20, caps=CEILING_CAPS):
     chunks = -(-wl.K // nb) * nb * rec                           # per instance, blocks of nb arms
     by_cap = {}
     for cap in caps:
+        if rest_s > 0:
+            time.sleep(rest_s)
         r_us, rw_us = ctypes.c_double(), ctypes.c_double()
         code = f(wl.B, chunks, rec, launches, cap, ctypes.byref(r_us), ctypes.byref(rw_us))
         if code == 3:      # the device's occupancy calculator does not confirm this cap
@@ -424,19 +427,18 @@ def main():
     head = measure(wl, K, W, dev, draws=draws)
     copy_gbs = copy_rate(dev, 3 if args.calibrate_copy else 5)
     torch.cuda.synchronize()
-    # the stream ceiling right after the headline's run and again after a
-    # second of idle: a busy device settles a few percent below the rate it
-    # starts at and recovers within half a second, so the step kernel is
-    # compared with the faster of the two (run before the headline, the
-    # ceiling's own load would slow the headline down)
+    # the stream ceiling right after the headline's run and again with a
+    # second of idle before each cap: a busy device settles a few percent
+    # below the rate it starts at and recovers within half a second, so the
+    # step kernel is compared with the faster of the two (run before the
+    # headline, the ceiling's own load would slow the headline down)
     ceil_busy = ceil_idle = None
     ceil_error = None
     if not args.no_ceiling:
         # a side measurement: if it cannot run, the line says why and stands
         try:
             ceil_busy = stream_ceiling(wl)
-            time.sleep(1.0)
-            ceil_idle = stream_ceiling(wl)
+            ceil_idle = stream_ceiling(wl, rest_s=1.0)
         except (OSError, RuntimeError) as exc:
             ceil_busy = ceil_idle = None
             ceil_error = str(exc)
@@ -488,7 +490,7 @@ def main():
                      f"per instance, non-temporal loads and stores; average of {c0['launches']} launches "
                      f"at each cap on workgroups per compute unit in {list(CEILING_CAPS)} (0: none; "
                      f"durations in us by cap), the fastest kept; measured right after the headline run "
-                     f"and again after 1 s of idle, the faster of the two reported")}
+                     f"and again with 1 s of idle before each cap, the faster of the two reported")}
     if not args.no_workloads:
         runs = {}
         for name in DETAIL_WORKLOADS:
