@@ -1555,8 +1555,8 @@ T *at(char *base, size_t off) {
 // workgroups (allocation granules round a request up).  Worked out once per
 // kernel and device; a share the calculator does not confirm, or below what
 // the kernel needs, leaves the launch uncapped.  Only host queries, no
-// allocation; a failed query is cleared so that the launch's own error check
-// does not see it.
+// allocation; the error of a failed query is cleared so that the launch's
+// own error check does not see it.
 constexpr int kMaxDevices = 64;
 template <int D, int TF, int W, int NW, bool ENV>
 std::atomic<int64_t> *capped_lds_cache() {
@@ -1567,24 +1567,29 @@ std::atomic<int64_t> *capped_lds_cache() {
 size_t capped_lds(const void *kernel, int threads, size_t need, int cap, std::atomic<int64_t> *cache) {
     if (cap <= 0) return need;
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    if (hipGetDevice(&dev) != hipSuccess) {
         (void)hipGetLastError();
         return need;
     }
+    if (dev < 0 || dev >= kMaxDevices) return need;
     int64_t v = cache[dev].load(std::memory_order_relaxed);
     if (v == 0) {
         int64_t dyn = 0;   // 0: uncapped
         int per_cu = 0;
         hipFuncAttributes fa;
-        if (hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) == hipSuccess &&
-            hipFuncGetAttributes(&fa, kernel) == hipSuccess && per_cu > 0) {
+        bool failed = hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+                          hipSuccess ||
+                      hipFuncGetAttributes(&fa, kernel) != hipSuccess;
+        if (!failed && per_cu > 0) {
             const int64_t max_dyn = 64 * 1024 - (int64_t)fa.sharedSizeBytes;
-            for (int64_t d = (per_cu / cap - (int64_t)fa.sharedSizeBytes) / 16 * 16;
-                 d >= (int64_t)need && d > 0; d -= 512) {
-                int blocks = 0;
+            for (int64_t d = (per_cu / cap - (int64_t)fa.sharedSizeBytes) / 16 * 16; d >= (int64_t)need && d > 0;
+                 d -= 512) {
                 if (d > max_dyn) continue;
-                if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, threads, (size_t)d) != hipSuccess)
+                int blocks = 0;
+                if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&blocks, kernel, threads, (size_t)d) != hipSuccess) {
+                    failed = true;
                     break;
+                }
                 if (blocks == cap) {
                     dyn = d;
                     break;
@@ -1592,7 +1597,7 @@ size_t capped_lds(const void *kernel, int threads, size_t need, int cap, std::at
                 if (blocks > cap) break;
             }
         }
-        (void)hipGetLastError();
+        if (failed) (void)hipGetLastError();
         v = dyn + 1;
         cache[dev].store(v, std::memory_order_relaxed);
     }
