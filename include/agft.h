@@ -245,7 +245,10 @@ int agft_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32_t
  * cap on workgroups per compute unit. */
 typedef struct agft_launch_shape {
     int32_t waves;        /* wavefronts per workgroup: 1 up to 16 KB streamed per
-                             instance, 4 beyond */
+                             instance, 4 beyond (with the switch: the exploiting
+                             instance's bytes; agft_step's steps before round
+                             ph_min_rounds, when no instance can exploit yet,
+                             take the exploring instance's width) */
     int32_t simd_waves;   /* wavefronts per SIMD the kernel's registers allow */
     int32_t tail_floats;  /* record layout, as agft_state_view.tail_floats */
     int32_t early_update; /* 1: the rank-1 update runs while the stream's first pass

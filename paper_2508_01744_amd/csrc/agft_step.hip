@@ -324,6 +324,17 @@ int waves_for(const agft_config &c) {
     return bytes <= 16384 ? 1 : 4;
 }
 
+// Before round ph_min_rounds no instance can have switched to exploitation,
+// so with the switch on, those steps take the width of an exploring
+// instance.  Measured on MI355X (us per step over the whole horizon, one
+// width throughout / exploring width before the first possible switch):
+// K=128 d=16 B=65,536 566.2 / 557.9, the same with rules 2-8 570.8 / 565.1,
+// B=16,384 82.6 / 81.5.
+int waves_at(const agft_config &c, int64_t t) {
+    if (c.exploit && t < c.ph_min_rounds) return explore_bytes(c) <= 16384 ? 1 : 4;
+    return waves_for(c);
+}
+
 // Whether the update of the previous decision's arm runs before the stream
 // (its first pass lands meanwhile and the chain gets shorter) rather than
 // after it: always, except at d = 32 where an instance streams more than
@@ -1663,7 +1674,7 @@ int launch_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32
     p.t_next = d_ctx != nullptr ? t + 1 : t;
     agft_launch_shape shape;
     agft_launch_shape_for(&c, &shape);
-    const int waves = shape.waves;
+    const int waves = waves_at(c, t);
     p.early_update = shape.early_update;
     p.keep_stats = stats_kept(c) ? 1 : 0;
     if (waves != 1 && waves != 4) return AGFT_E_UNSUPPORTED;
@@ -1677,7 +1688,7 @@ int launch_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32
     // the end of each workgroup wants more instances in flight (K=128 d=16,
     // us per fused step, uncapped / at 4: B=65,536 881.5 / 891.0, B=16,384
     // 211.9 / 218.0).
-    const int cap = env != nullptr ? 0 : shape.cu_workgroups;
+    const int cap = env != nullptr ? 0 : cu_workgroups_for(waves, shape.simd_waves);
 #define AGFT_LAUNCH(D_, TF_, W_)                                                       \
     (env != nullptr ? launch_width<D_, TF_, W_, true>(waves, cap, grid, lds, s, p, e) \
                     : launch_width<D_, TF_, W_, false>(waves, cap, grid, lds, s, p, e))
