@@ -1612,7 +1612,8 @@ size_t capped_lds(const void *kernel, int threads, size_t need, int cap, std::at
         v = dyn + 1;
         cache[dev].store(v, std::memory_order_relaxed);
     }
-    return v > 1 ? (size_t)(v - 1) : need;
+    // (a share worked out for a smaller need than this launch's is not used)
+    return v > 1 && (size_t)(v - 1) >= need ? (size_t)(v - 1) : need;
 }
 
 template <int D, int TF, int W, bool ENV>
