@@ -472,6 +472,10 @@ def main():
                                         "mean_active_arms_after_step", "exploiting_fraction", "wall_s")},
     }
     res["detail"]["device_copy_gbs"] = copy_gbs
+    # how agft_step launches the headline's step kernel (the first rounds of a
+    # workload with the switch take the exploring width)
+    from paper_2508_01744_amd import launch_shape, workload_config
+    res["detail"]["launch_shape"] = launch_shape(workload_config(wl))
     if ceil_error is not None:
         res["roofline"]["ceiling"] = {"error": ceil_error}
     if ceil_busy is not None:
