@@ -88,14 +88,25 @@ class TimingEvent:
 
 def counter_traffic(workload, path=COUNTERS, source=STEP_SRC, steps=None, warmup=None):
     """HBM bytes per step-kernel launch from the committed counter summary,
-    or None unless it was taken on this workload with this kernel source and
-    over the same window (timed steps after warm-up steps) as this run."""
+    or None unless it was taken on this workload with this kernel source.
+
+    The summary holds the bytes of every step of a fresh run
+    (per_step_hbm_bytes[t], t = 0, 1, ...): a bench run times its steps from
+    a fresh state on the same draws, so its window is the first `steps` of
+    them, whatever its warm-up (None if the summary covers fewer steps).  A
+    summary with one figure for a window (steps, warmup) serves only that
+    window."""
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         cnt = json.load(fh)
     if cnt.get("source_sha256_16") != source_hash(source) or cnt.get("workload") != workload:
         return None
+    per_step = cnt.get("per_step_hbm_bytes")
+    if per_step is not None:
+        if steps is None:
+            return None
+        return sum(per_step[:steps]) / steps if 0 < steps <= len(per_step) else None
     if steps is not None and (cnt.get("steps"), cnt.get("warmup")) != (steps, warmup):
         return None
     return cnt.get("hbm_bytes_per_launch")
@@ -462,9 +473,10 @@ def main():
                    "context_dim": wl.d, "steps_per_run": wl.T, "parallelism": "none (1 GPU)"},
         "roofline": {"bound": "hbm", "achieved": head["achieved_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": head["frac"], "traffic": traffic,
-                     "traffic_window": (f"HBM bytes per step-kernel launch over the same {K} timed steps "
-                                        f"(after {W} warm-up steps) of {wl.name}, from rocprofv3 counters "
-                                        f"on this kernel source" if traffic is not None else None),
+                     "traffic_window": (f"HBM bytes per step-kernel launch averaged over the {K} timed steps "
+                                        f"of {wl.name} (the first {K} from a fresh state), from per-step "
+                                        f"rocprofv3 counters on this kernel source"
+                                        if traffic is not None else None),
                      "byte_model": byte_model(wl)},
         "detail": {k: head[k] for k in ("step_kernel_avg_ms", "step_kernel_median_ms", "step_kernel_share",
                                         "ms_per_step_fused",

@@ -62,6 +62,13 @@ def test_traffic_only_for_the_profiled_source_and_workload(tmp_path):
     assert bench.counter_traffic("cfg4", str(path), str(src), steps=20, warmup=5) == 5.1e9
     assert bench.counter_traffic("cfg4", str(path), str(src), steps=500, warmup=5) is None
     assert bench.counter_traffic("cfg4", str(path), str(src), steps=20, warmup=20) is None
+    # per-step counters of a fresh run serve any window within them: the mean
+    # of its first `steps` steps, whatever the warm-up
+    write(per_step_hbm_bytes=[5.0e9, 5.2e9, 5.4e9, 5.6e9])
+    assert bench.counter_traffic("cfg4", str(path), str(src), steps=2, warmup=5) == 5.1e9
+    assert abs(bench.counter_traffic("cfg4", str(path), str(src), steps=4, warmup=20) - 5.3e9) < 1.0
+    assert bench.counter_traffic("cfg4", str(path), str(src), steps=5, warmup=5) is None
+    assert bench.counter_traffic("cfg4", str(path), str(src)) is None
     write()
     src.write_text("kernel source, changed\n")
     assert bench.counter_traffic("cfg4", str(path), str(src)) is None
