@@ -268,8 +268,9 @@ def measure(wl, K, W, dev, log_prefix="[bench]", draws=None):
     elapsed_ms = start.elapsed_time(stop)
     kernel_ms = np.array([a.elapsed_time(b) for a, b in ev])
 
-    # the same steps with the decision and the environment's response fused
-    # into one launch per step (agft_sim_step)
+    # the same steps through agft_sim_step (the environment in the step
+    # kernel's epilogue, one launch per step, up to 8,192 instances; the two
+    # kernels above)
     fresh()
     torch.cuda.synchronize()
     f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -524,8 +525,9 @@ def main():
             for name, r in runs.items()}
         res["detail"]["workloads_note"] = ("each workload timed over its whole horizon from a fresh state, "
                                            "step and environment kernels, inputs resident; *_fused: the same "
-                                           "steps with the environment in the step kernel's epilogue "
-                                           "(agft_sim_step, one launch per step); frac = algorithmic bytes per "
+                                           "steps through agft_sim_step (the environment in the step kernel's "
+                                           "epilogue, one launch per step, up to 8,192 instances; the step "
+                                           "and environment kernels above); frac = algorithmic bytes per "
                                            "step-kernel launch over its average duration, of 8 TB/s")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")

@@ -255,7 +255,7 @@ typedef struct agft_launch_shape {
                              is in flight; 0: after the stream */
     int32_t cu_workgroups;  /* workgroups per compute unit agft_step's launch admits
                                (its LDS request caps them there); 0: no cap.
-                               agft_sim_step launches uncapped. */
+                               agft_sim_step's single launch is uncapped. */
 } agft_launch_shape;
 
 /* Fill *out for cfg.  AGFT_E_INVAL if cfg is invalid or out is NULL,

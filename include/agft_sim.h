@@ -81,17 +81,18 @@ int agft_env_step(const agft_env_config *cfg, void *d_env, size_t nbytes, int32_
                   float *d_reward, float *d_ctx, void *stream);
 
 /*
- * One decision of tuner h followed by the environment's response, in a
- * single launch: the same results as
+ * One decision of tuner h followed by the environment's response: the same
+ * results as
  *   agft_step(h, d_ctx, d_reward, d_action, d_scores);
  *   agft_env_step(env_cfg, d_env, env_nbytes, t, d_action, d_arrivals, d_noise,
  *                 d_reward, d_ctx, stream of h);
- * with t the decisions h had made before the call, each instance's
- * environment running in the step's epilogue once its decision is known
- * (the decision step of Sec. 4.2 followed by the measured window of Sec. 4.1,
- * without the second launch and its wait).  In place: d_ctx holds x_t on
- * entry and x_{t+1} on return, d_reward r_{t-1} (read only when a decision
- * is pending) and then r_t.  Enqueued on h's stream.
+ * with t the decisions h had made before the call (the decision step of
+ * Sec. 4.2 followed by the measured window of Sec. 4.1).  Up to 8,192
+ * instances in a single launch, each instance's environment running in the
+ * step's epilogue once its decision is known, without the second launch and
+ * its wait; beyond that as the two calls above, which are faster there.
+ * In place: d_ctx holds x_t on entry and x_{t+1} on return, d_reward r_{t-1}
+ * (read only when a decision is pending) and then r_t.  Enqueued on h's stream.
  * env_cfg must describe the same B, K, d as h; d_env as in agft_env_step.
  * d_ctx [B][d] fp32 (16-byte aligned), d_reward [B] fp32, d_action [B] int32:
  * device, non-NULL.  d_scores [B][2][K] or NULL, as in agft_step.

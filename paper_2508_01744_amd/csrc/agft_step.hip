@@ -1569,6 +1569,8 @@ T *at(char *base, size_t off) {
 // allocation; the error of a failed query is cleared so that the launch's
 // own error check does not see it.
 constexpr int kMaxDevices = 64;
+// agft_sim_step runs the environment in the step kernel's epilogue up to this many instances
+constexpr int kFusedMaxB = 8192;
 template <int D, int TF, int W, int NW, bool ENV>
 std::atomic<int64_t> *capped_lds_cache() {
     static std::atomic<int64_t> cache[kMaxDevices];   // 0: not worked out; else bytes + 1
@@ -1827,6 +1829,19 @@ int agft_sim_step(agft_handle *h, const agft_env_config *env_cfg, void *d_env, s
     const double tau = env_cfg->T > 1 ? (double)h->t / (double)(env_cfg->T - 1) : 0.0;
     e.scale = (float)(1.0 + (double)env_cfg->drift * tau);
     e.reset = 0;
+    // Large batches take the step kernel and then the environment kernel:
+    // there the epilogue's per-instance stores to the environment's
+    // structure-of-arrays state cost more than the launch they save.
+    // Measured on MI355X (us per simulator step over the whole horizon,
+    // fused / two launches): K=128 d=16 B=65,536 884 / 819, B=16,384 212 /
+    // 203; K=64 d=8 B=4,096 16.1 / 18.5; K=256 d=32 B=1,024 23.4 / 26.5.
+    if (h->cfg.B > kFusedMaxB) {
+        const int64_t t = h->t;
+        const int rc = launch_step(h, d_ctx, d_reward, d_action, d_scores, nullptr);
+        if (rc != AGFT_OK) return rc;
+        return agft_env_step(env_cfg, d_env, env_nbytes, (int32_t)t, d_action, d_arrivals, d_noise, d_reward, d_ctx,
+                             h->stream);
+    }
     return launch_step(h, d_ctx, d_reward, d_action, d_scores, &e);
 }
 

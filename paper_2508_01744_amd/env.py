@@ -68,8 +68,9 @@ class GpuEnv:
 
     def fused_step(self, tuner, action, scores=None):
         """One decision of tuner (agft_step) and this environment's response
-        to it, in one launch (agft_sim_step): self.ctx and self.reward hold
-        x_t and r_{t-1} on entry and x_{t+1} and r_t on return."""
+        to it (agft_sim_step: one launch up to 8,192 instances, the step and
+        environment kernels above): self.ctx and self.reward hold x_t and
+        r_{t-1} on entry and x_{t+1} and r_t on return."""
         tuner._check(action, (self.B,), torch.int32)
         tuner._check(scores, (self.B, 2, tuner.K), torch.float32)
         L.check("agft_sim_step", L.agft_sim_step(tuner.h, self.cfg, _ptr(self.state), self.nbytes,

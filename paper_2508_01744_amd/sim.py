@@ -11,8 +11,9 @@ def run_closed_loop(wl, env_constants, arrivals, noise, T=None, probes=None, sco
     """Run T decisions of wl.B instances.
 
     arrivals, noise: [T+1][B] (numpy or torch) exogenous draws.
-    fused: each decision and the environment's response in one launch
-    (agft_sim_step) instead of two (agft_step, agft_env_step).
+    fused: each decision and the environment's response through
+    agft_sim_step (one launch up to 8,192 instances) instead of agft_step
+    and agft_env_step.
     probes: instance indices to record at every step (contexts, rewards,
     actions, masks, test words, action spaces; with scores, the scores and
     the top-two gap of each decision); the records are returned as host

@@ -1,6 +1,6 @@
 """The simulator's fused step (agft_sim_step: the decision and the
-environment's response in one launch) against the two separate calls it
-replaces, and against the oracle.
+environment's response in one launch, up to 8,192 instances) against the two
+separate calls it replaces, and against the oracle.
 
 Fused and separate runs of the same workload must agree bit for bit:
 contexts, rewards, actions, masks, scores, top-two gaps and the final state
@@ -31,6 +31,24 @@ def test_fused_equals_separate(name):
     say(f"[fused] {wl.name} B={wl.B} K={wl.K} d={wl.d} T={wl.T}")
     arr, noi = exogenous(wl)
     ids = list(range(wl.B))
+    sep = run_closed_loop(wl, ENV, arr, noi, probes=ids, scores=True)
+    fus = run_closed_loop(wl, ENV, arr, noi, probes=ids, scores=True, fused=True)
+    for key in sep["probes"]:
+        a, b = sep["probes"][key], fus["probes"][key]
+        assert torch.equal(a.view(torch.int32) if a.is_floating_point() else a,
+                           b.view(torch.int32) if b.is_floating_point() else b), key
+    assert torch.equal(sep["tuner"].state, fus["tuner"].state)
+    assert torch.equal(sep["env"].state, fus["env"].state)
+
+
+def test_large_batch_simulator_step_equals_separate():
+    """Above 8,192 instances agft_sim_step runs the step kernel and then the
+    environment kernel: the same results as the separate calls, bit for bit,
+    and the same in-place buffers (one instance past the threshold)."""
+    wl = get_workload("cfg3", B=8193, T=40)
+    say(f"[fused] two launches: {wl.name} B={wl.B} K={wl.K} d={wl.d} T={wl.T}")
+    arr, noi = exogenous(wl)
+    ids = [0, 1, 4096, 8191, 8192]
     sep = run_closed_loop(wl, ENV, arr, noi, probes=ids, scores=True)
     fus = run_closed_loop(wl, ENV, arr, noi, probes=ids, scores=True, fused=True)
     for key in sep["probes"]:
