@@ -1819,6 +1819,19 @@ int agft_sim_step(agft_handle *h, const agft_env_config *env_cfg, void *d_env, s
     if (reinterpret_cast<uintptr_t>(d_env) % agft_env_detail::kAlign != 0 || env_nbytes < env_layout(env_cfg->B).total)
         return AGFT_E_INVAL;
     if (h->t >= env_cfg->T) return AGFT_E_STATE;   // the draws end at window T
+    // Large batches take the step kernel and then the environment kernel:
+    // there the epilogue's per-instance stores to the environment's
+    // structure-of-arrays state cost more than the launch they save.
+    // Measured on MI355X (us per simulator step over the whole horizon,
+    // fused / two launches): K=128 d=16 B=65,536 879 / 814, B=16,384 211 /
+    // 201; K=64 d=8 B=4,096 16.1 / 18.5; K=256 d=32 B=1,024 23.4 / 27.1.
+    if (h->cfg.B > kFusedMaxB) {
+        const int64_t t = h->t;
+        const int rc = launch_step(h, d_ctx, d_reward, d_action, d_scores, nullptr);
+        if (rc != AGFT_OK) return rc;
+        return agft_env_step(env_cfg, d_env, env_nbytes, (int32_t)t, d_action, d_arrivals, d_noise, d_reward, d_ctx,
+                             h->stream);
+    }
     EnvArgs e = make_args(env_cfg, d_env);
     e.arrivals = d_arrivals;
     e.noise = d_noise;
@@ -1829,19 +1842,6 @@ int agft_sim_step(agft_handle *h, const agft_env_config *env_cfg, void *d_env, s
     const double tau = env_cfg->T > 1 ? (double)h->t / (double)(env_cfg->T - 1) : 0.0;
     e.scale = (float)(1.0 + (double)env_cfg->drift * tau);
     e.reset = 0;
-    // Large batches take the step kernel and then the environment kernel:
-    // there the epilogue's per-instance stores to the environment's
-    // structure-of-arrays state cost more than the launch they save.
-    // Measured on MI355X (us per simulator step over the whole horizon,
-    // fused / two launches): K=128 d=16 B=65,536 884 / 819, B=16,384 212 /
-    // 203; K=64 d=8 B=4,096 16.1 / 18.5; K=256 d=32 B=1,024 23.4 / 26.5.
-    if (h->cfg.B > kFusedMaxB) {
-        const int64_t t = h->t;
-        const int rc = launch_step(h, d_ctx, d_reward, d_action, d_scores, nullptr);
-        if (rc != AGFT_OK) return rc;
-        return agft_env_step(env_cfg, d_env, env_nbytes, (int32_t)t, d_action, d_arrivals, d_noise, d_reward, d_ctx,
-                             h->stream);
-    }
     return launch_step(h, d_ctx, d_reward, d_action, d_scores, &e);
 }
 
