@@ -14,7 +14,8 @@
  * enqueues work on the handle's HIP stream and returns without waiting,
  * except agft_create with AGFT_ADOPT_STATE, which reads the buffer's header
  * back synchronously.  A handle is not thread-safe; use one handle per
- * stream.
+ * stream.  Calls launch on the calling thread's current HIP device: make
+ * the device of the handle's stream and buffers current before each call.
  *
  * Errors: every int-returning call returns AGFT_OK (0) or a negative code;
  * arguments are validated before anything is enqueued.  A device fault of

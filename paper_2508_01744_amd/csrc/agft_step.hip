@@ -1557,9 +1557,10 @@ template <class T>
 T *at(char *base, size_t off) {
     return reinterpret_cast<T *>(base + off);
 }
+// agft_sim_step runs the environment in the step kernel's epilogue up to
+// this many instances, and launches the step and environment kernels above.
+constexpr int kFusedMaxB = 8192;
 
-// The step kernel for one or four wavefronts per workgroup (the two widths
-// waves_for chooses), each compiled for its width.
 // Dynamic LDS that caps a kernel at `cap` workgroups per compute unit: a
 // 1/cap share of the unit's LDS less the kernel's static LDS, lowered in
 // 512-byte steps until the occupancy calculator admits exactly cap
@@ -1569,8 +1570,6 @@ T *at(char *base, size_t off) {
 // allocation; the error of a failed query is cleared so that the launch's
 // own error check does not see it.
 constexpr int kMaxDevices = 64;
-// agft_sim_step runs the environment in the step kernel's epilogue up to this many instances
-constexpr int kFusedMaxB = 8192;
 template <int D, int TF, int W, int NW, bool ENV>
 std::atomic<int64_t> *capped_lds_cache() {
     static std::atomic<int64_t> cache[kMaxDevices];   // 0: not worked out; else bytes + 1
@@ -1618,6 +1617,8 @@ size_t capped_lds(const void *kernel, int threads, size_t need, int cap, std::at
     return v > 1 && (size_t)(v - 1) >= need ? (size_t)(v - 1) : need;
 }
 
+// The step kernel for one or four wavefronts per workgroup (the two widths
+// waves_for chooses), each compiled for its width.
 template <int D, int TF, int W, bool ENV>
 void launch_width(int waves, int cap, unsigned grid, size_t lds, hipStream_t stream, const StepArgs &p,
                   const agft_env_detail::EnvArgs &e) {
@@ -1687,9 +1688,10 @@ int launch_step(agft_handle *h, const float *d_ctx, const float *d_reward, int32
     hipStream_t s = h->stream;
     agft_env_detail::EnvArgs e{};
     if (env != nullptr) e = *env;
-    // The simulator's step launches uncapped: the environment's response at
-    // the end of each workgroup wants more instances in flight (K=128 d=16,
-    // us per fused step, uncapped / at 4: B=65,536 881.5 / 891.0, B=16,384
+    // The simulator's single launch runs uncapped: the environment's
+    // response at the end of each workgroup wants more instances in flight
+    // (K=128 d=16, us per fused step, uncapped / at 4, measured when larger
+    // batches took the single launch too: B=65,536 881.5 / 891.0, B=16,384
     // 211.9 / 218.0).
     const int cap = env != nullptr ? 0 : cu_workgroups_for(waves, shape.simd_waves);
 #define AGFT_LAUNCH(D_, TF_, W_)                                                       \
