@@ -509,26 +509,44 @@ def main():
                      f"durations in us by cap), the fastest kept; measured right after the headline run "
                      f"and again with 1 s of idle before each cap, the faster of the two reported")}
     if not args.no_workloads:
-        runs = {}
+        runs, ceilings = {}, {}
+        if "ceiling" in res["roofline"] and "read_writeback_gbs" in res["roofline"]["ceiling"]:
+            ceilings[wl.name] = res["roofline"]["ceiling"]["read_writeback_gbs"]
         for name in DETAIL_WORKLOADS:
+            w2 = get_workload(name)
             if name == wl.name and args.steps is None:
                 runs[name] = head
-                continue
-            w2 = get_workload(name)
-            runs[name] = measure(w2, w2.T, W, dev, log_prefix="[bench detail]",
-                                 draws=draws if name == wl.name else None)
+            else:
+                runs[name] = measure(w2, w2.T, W, dev, log_prefix="[bench detail]",
+                                     draws=draws if name == wl.name else None)
+            # the stream ceiling on this workload's layout, as for the headline
+            # (the faster of right after its run and rested); not for a single
+            # instance, whose launch is all latency
+            if not args.no_ceiling and name not in ceilings and w2.B > 1:
+                try:
+                    c0 = stream_ceiling(w2)
+                    c1 = stream_ceiling(w2, rest_s=0.5)
+                    ceilings[name] = max(c0["read_writeback_gbs"], c1["read_writeback_gbs"])
+                except (OSError, RuntimeError) as exc:
+                    log(f"[bench detail] {name}: stream ceiling not measured: {exc}")
         res["detail"]["workloads"] = {
             name: {"steps": r["steps"], "decision_steps_per_s": r["value"], "ms_per_step": r["ms_per_step"],
                    "decision_steps_per_s_fused": r["value_fused"], "ms_per_step_fused": r["ms_per_step_fused"],
                    "step_kernel_avg_ms": r["step_kernel_avg_ms"], "achieved_gbs": r["achieved_gbs"],
-                   "frac": r["frac"], "mean_scored_arms": r["mean_scored_arms"]}
+                   "frac": r["frac"], "mean_scored_arms": r["mean_scored_arms"],
+                   "ceiling_read_writeback_gbs": ceilings.get(name),
+                   "of_ceiling": r["achieved_gbs"] / ceilings[name] if name in ceilings else None}
             for name, r in runs.items()}
         res["detail"]["workloads_note"] = ("each workload timed over its whole horizon from a fresh state, "
                                            "step and environment kernels, inputs resident; *_fused: the same "
                                            "steps through agft_sim_step (the environment in the step kernel's "
                                            "epilogue, one launch per step, up to 8,192 instances; the step "
                                            "and environment kernels above); frac = algorithmic bytes per "
-                                           "step-kernel launch over its average duration, of 8 TB/s")
+                                           "step-kernel launch over its average duration, of 8 TB/s; "
+                                           "of_ceiling = the same rate over the stream ceiling's "
+                                           "read-plus-write-back rate on the workload's record layout "
+                                           "(measured as for the headline; the headline's own for its "
+                                           "workload; none for a single instance)")
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host")
         base = cpu_baseline(wl, args.cpu_budget)

@@ -68,3 +68,12 @@ def test_bench_json_line():
         steps = {"cfg1": 10000, "cfg2": 2000, "cfg3": 1000, "cfg4": 500, "cfg5": 2000}[name]
         assert w["steps"] == steps and w["decision_steps_per_s"] > 0 and 0 < w["frac"] < 1.5
         assert 0 < w["step_kernel_avg_ms"] < w["ms_per_step"] and w["mean_scored_arms"] > 0
+        # the stream ceiling on each workload's layout (the headline's own for
+        # cfg2), none for the single instance of cfg1
+        if name == "cfg1":
+            assert w["ceiling_read_writeback_gbs"] is None and w["of_ceiling"] is None
+        else:
+            assert w["ceiling_read_writeback_gbs"] > 0
+            assert abs(w["of_ceiling"] - w["achieved_gbs"] / w["ceiling_read_writeback_gbs"]) < 1e-9
+            assert 0 < w["of_ceiling"] < 1.2
+    assert wls["cfg2"]["ceiling_read_writeback_gbs"] == ce["read_writeback_gbs"]
