@@ -268,16 +268,22 @@ size_t explore_bytes(const agft_config &c) {
 }
 
 // Record layout: packed tails (TF = 3) where an exploring instance streams
-// more than 16 KB per step, so that the stream moves no padding; padded
-// tails (TF = 4) otherwise, where the update's one-record read and
-// write-back weigh more than the stream and a tail that straddles two
-// lines costs more than its padding.  Measured on MI355X (step kernel,
-// packed / padded tails): K=128 d=16 B=65,536 (76 KB) 853 / 889 us, the
-// same with exploitation 827 / 845 us, K=256 d=32 B=1,024 (560 KB) 92.0 /
-// 93.0 us; K=64 d=8 B=4,096 (11 KB) 18.8 / 18.3 us, K=128 d=16 B=65,536
-// with the refinement (13 KB) 186 / 176 us, with the refinement, the rules
-// and the switch 190 / 179 us.
-int tail_floats(const agft_config &c) { return explore_bytes(c) > 16384 ? 3 : 4; }
+// more than 16 KB per step, or more than 8 KB when every step streams every
+// record (no pruning rule, no refinement, no switch to exploitation), so
+// that the stream moves no padding; padded tails (TF = 4) otherwise, where
+// the update's one-record read and write-back weigh more than the stream
+// and a tail that straddles two lines costs more than its padding.
+// Measured on MI355X (step kernel, packed / padded tails): K=128 d=16
+// B=65,536 (76 KB) 853 / 889 us, the same with exploitation 827 / 845 us,
+// K=256 d=32 B=1,024 (560 KB) 92.0 / 93.0 us, K=128 d=16 B=65,536 with the
+// refinement (13 KB) 186 / 176 us, with the refinement, the rules and the
+// switch 190 / 179 us; K=64 d=8 B=4,096 (11 KB) over the whole horizon
+// 12.85 / 13.25 us without pruning, 11.6 / 11.25 us with rules 1-8,
+// 10.45 / 10.45 us with the refinement, 10.5 / 10.4 us with the switch.
+int tail_floats(const agft_config &c) {
+    const size_t bytes = explore_bytes(c);
+    return bytes > 16384 || (bytes > 8192 && c.prune_rule == 0 && !c.refine && !c.exploit) ? 3 : 4;
+}
 
 // The per-arm reward counts and sums are read only by the paper's rules 2-8
 // and by the refinement's statistical anchor; without those the update

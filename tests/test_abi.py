@@ -64,11 +64,18 @@ def test_state_bytes(lib):
     # K is rounded up to whole blocks of 64/d arms: K=125 at d=16 takes 128 slots
     # (the other regions of K=125 add less than the 3 slots' 7.5 MB)
     assert L.agft_state_bytes(_cfg(B=4096, K=125, d=16)) >= 4096 * 128 * 38 * 16
-    # up to 16 KB of records per exploring instance (26 arms of 608 bytes at
-    # d=16) the tails are padded to whole chunks: 40 chunks per record, so
-    # K=26 (28 slots of 640 bytes) needs more than K=27 (28 slots of 608)
-    b26, b27 = (L.agft_state_bytes(_cfg(B=4096, K=k, d=16)) for k in (26, 27))
+    # with pruning, up to 16 KB of records per exploring instance (26 arms of
+    # 608 bytes at d=16) the tails are padded to whole chunks: 40 chunks per
+    # record, so K=26 (28 slots of 640 bytes) needs more than K=27 (28 slots
+    # of 608)
+    b26, b27 = (L.agft_state_bytes(_cfg(B=4096, K=k, d=16, prune_rule=1)) for k in (26, 27))
     assert 4096 * 28 * 40 * 16 <= b26 and b27 < b26 and b27 - 4096 * 28 * 38 * 16 < 4096 * (27 * 8 + 272) + 1024
+    # without pruning or refinement every step streams every record: packed
+    # tails from 8 KB (14 arms at d=16), so K=26 takes the 608-byte records
+    p26 = L.agft_state_bytes(_cfg(B=4096, K=26, d=16))
+    assert p26 < b26 and 0 <= p26 - 4096 * 28 * 38 * 16 < 4096 * (26 * 8 + 272) + 1024
+    b13, b14 = (L.agft_state_bytes(_cfg(B=4096, K=k, d=16)) for k in (13, 14))
+    assert b13 - 4096 * 16 * 40 * 16 >= 0 and b14 < b13
     # the refinement counts the arms in play: K=128 with windows of 21 arms
     # and a coarse grid of 13 streams 12.8 KB, padded tails
     ref = dict(refine=1, refine_period=50, refine_stride=10, refine_half=10, refine_mature=100,

@@ -43,8 +43,9 @@ def test_bench_json_line():
     assert cb["cores"] >= 1 and "cfg2" in cb["sample"]
     assert det["cpu_oracle_1thread"]["cores"] == 1
     assert det["host_cpu"]["cpus_visible"] >= 1 and "model" in det["host_cpu"]
-    # cfg2: one-wavefront workgroups, padded tails, no cap on workgroups per compute unit
-    assert det["launch_shape"] == {"waves": 1, "simd_waves": 7, "tail_floats": 4, "early_update": 1,
+    # cfg2: one-wavefront workgroups, packed tails (nothing prunes its arms),
+    # no cap on workgroups per compute unit
+    assert det["launch_shape"] == {"waves": 1, "simd_waves": 7, "tail_floats": 3, "early_update": 1,
                                    "cu_workgroups": 0}
     assert rf["byte_model"]["model_bytes_per_arm"] == 176 and rf["byte_model"]["dense_bytes_per_arm"] == 288
     # the stream ceiling on cfg2's layout: reading alone is faster than

@@ -13,7 +13,7 @@ from paper_2508_01744_amd import launch_shape, make_config, workload_config
 # workload: (wavefronts per workgroup, wavefronts per SIMD, tail floats, early
 # update, workgroups per compute unit)
 EXPECTED = {
-    "cfg1": (1, 7, 4, 1, 0), "cfg2": (1, 7, 4, 1, 0), "cfg3": (4, 6, 3, 1, 4), "cfg4": (4, 6, 3, 1, 4),
+    "cfg1": (1, 7, 4, 1, 0), "cfg2": (1, 7, 3, 1, 0), "cfg3": (4, 6, 3, 1, 4), "cfg4": (4, 6, 3, 1, 4),
     "cfg5": (4, 4, 3, 0, 0),
     "cfg2p": (1, 7, 4, 1, 0), "cfg3p": (4, 7, 3, 1, 0), "cfg4p": (4, 7, 3, 1, 0), "cfg5p": (4, 4, 3, 0, 0),
     "cfg1e": (1, 7, 4, 1, 0), "cfg2e": (1, 7, 4, 1, 0), "cfg3e": (1, 6, 3, 1, 0), "cfg4e": (1, 6, 3, 1, 0),
@@ -36,6 +36,9 @@ def test_rules_at_their_thresholds():
         return launch_shape(make_config(**base))
     # 16 KB of records per exploring instance: 26 arms of 608 bytes at d = 16
     assert shape(K=26)["tail_floats"] == 4 and shape(K=27)["tail_floats"] == 3
+    # 8 KB where nothing prunes or restricts the arms: 13 and 14 arms at d = 16
+    assert shape(K=13, prune_rule=0)["tail_floats"] == 4 and shape(K=14, prune_rule=0)["tail_floats"] == 3
+    assert shape(K=14)["tail_floats"] == 4
     assert shape(K=26)["waves"] == 1 and shape(K=27)["waves"] == 4
     # the paper's rules keep seven wavefronts per SIMD at d = 16
     rules = dict(ext_rounds=60, ext_min_n=3, ext_thr=-1.2, hist_after=30, hist_min_n=6, hist_kappa=1.0,
