@@ -151,8 +151,10 @@ typedef struct agft_state_view {
     int32_t tail_floats;/* TF, floats per lane slice of a record tail: 3 (packed, no
                            padding) when an exploring instance streams more than
                            16 KB of records per step (arms in play * 4 * (d +
-                           d(d+1)/2) bytes), else 4 (one float of padding per slice,
-                           so that no tail straddles two 128-byte lines) */
+                           d(d+1)/2) bytes), or more than 8 KB with no pruning
+                           rule, refinement or switch to exploitation; else 4
+                           (one float of padding per slice, so that no tail
+                           straddles two 128-byte lines) */
     int32_t mask_words; /* uint32 words per instance in the action-set mask: ceil(K/32) */
     void *arms;         /* float4 records, instance i's at chunk i * ceil(K/NB)*NB*chunks.
                            Arm k sits in block k/NB (NB*chunks chunks), slot r = k%NB.

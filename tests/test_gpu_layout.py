@@ -1,7 +1,8 @@
-"""Both record layouts on the GPU against the oracle: packed tails (an
-exploring instance streams more than 16 KB of records per step) and tails
-padded to whole chunks (16 KB or less), at every supported d, with an arm
-count that leaves the last block of records part-filled.
+"""Both record layouts on the GPU against the oracle: packed tails (with
+pruning on, as here: an exploring instance streams more than 16 KB of
+records per step) and tails padded to whole chunks (16 KB or less), at every
+supported d, with an arm count that leaves the last block of records
+part-filled.
 
 Open loop (the same contexts and rewards to both sides); afterwards the
 final models are compared through the export kernel, and the raw records
